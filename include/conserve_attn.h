@@ -1,0 +1,196 @@
+/*
+ * conserve_attn.h -- C ABI of the paged-KV attention hot path under conversation-level
+ * disaggregated serving (arxiv 2606.01839, "Observation, Not Prediction").
+ *
+ * The paper (Section 4 and Fig. 9) binds each agentic conversation to one decoder for its whole
+ * life: the turn-1 prompt is prefilled (on the prefiller), the resulting KV cache is transferred
+ * exactly once, and the first decode plus every later turn's incremental prefill ("append") and
+ * decode run on the decoder against the conversation's ever-growing KV cache (Section 1; Section
+ * 3.1 "prefix caching" and "KV cache transfer"; Section 3.2 "memory-bound" decode). This library is
+ * the data-parallel part of that: a pool of 16-token KV pages per GPU, conversations that own pages,
+ * and the kernels that append KV, attend (turn-1 prefill, extend, batched decode) and move a
+ * conversation's KV out of / into a pool (the one-time transfer).
+ *
+ * Conventions for every call
+ * --------------------------
+ *  - Device pointers: every `void*` named k, v, q, out, dst, src, kv_base, ws_base is a device
+ *    address on the current HIP device; the caller owns that memory and keeps it alive until the
+ *    stream reaches the call. Host pointers: cs_conv arrays, q_lens, and the out-parameters.
+ *  - Element type: bf16 (IEEE binary32 with the low 16 bits dropped) everywhere; accumulation fp32.
+ *  - Append-then-attend: cs_kv_append is the only writer of a conversation's K/V. Attention calls
+ *    take queries for the LAST q_len positions of each conversation; query i of a conversation of
+ *    length L sits at position p = L - q_len + i and sees keys 0..p (itself included). Softmax
+ *    scale is exactly 1/sqrt(head_dim). Query head h reads KV head h / (n_q_heads / n_kv_heads).
+ *  - Errors: every call validates all arguments before changing any state; on error it returns a
+ *    negative cs_status, changes nothing, and sets a thread-local message (cs_last_error). Nothing
+ *    aborts or throws across this ABI. CS_EHIP reports a failing HIP runtime call; the pool may then
+ *    be inconsistent with the device and should be destroyed.
+ *  - Asynchrony: host metadata (lengths, page tables) is committed when the call returns; kernels
+ *    and the small metadata uploads they need are enqueued on `stream` (a hipStream_t, 0 = null
+ *    stream). No call synchronises the device, except that switching a pool to another stream
+ *    makes the new stream wait (hipStreamWaitEvent) for work already enqueued on the previous one.
+ *  - A pool is not thread-safe: one host thread at a time.
+ */
+#ifndef CONSERVE_ATTN_H
+#define CONSERVE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct cs_pool cs_pool;   /* opaque; library-owned host metadata */
+typedef int32_t cs_conv;          /* conversation handle (>= 0) */
+typedef void* cs_stream;          /* hipStream_t */
+typedef int32_t cs_status;
+
+enum {
+  CS_OK = 0,
+  CS_EINVAL = -1,  /* bad argument: null pointer, bad size, duplicate conversation, wire mismatch */
+  CS_ENOMEM = -2,  /* pool has too few free pages / no free conversation slot / ring too small */
+  CS_ENOENT = -3,  /* unknown or destroyed conversation handle */
+  CS_ESTATE = -4,  /* call not valid in the conversation's state (e.g. q_len > length) */
+  CS_ERANGE = -5,  /* index out of range (layer, page capacity of a conversation) */
+  CS_EHIP = -6     /* a HIP runtime call failed */
+};
+
+#define CS_PAGE_TOKENS 16
+
+typedef struct {
+  int32_t n_layers;            /* >= 1 */
+  int32_t n_q_heads;           /* multiple of n_kv_heads; n_q_heads/n_kv_heads in {1,2,4,8} */
+  int32_t n_kv_heads;          /* >= 1 */
+  int32_t head_dim;            /* 64 or 128 */
+  int32_t max_convs;           /* live conversations at once, 1 .. 2^20 */
+  int32_t max_pages_per_conv;  /* longest conversation, in 16-token pages */
+  int64_t n_pages;             /* pool capacity in pages; a page holds 16 tokens of every layer */
+} cs_pool_desc;
+
+/*
+ * KV pool layout (device, caller-allocated, cs_pool_kv_bytes(desc) bytes, 256-byte aligned):
+ *   pool[layer][page][kv_head] = one 4*16*head_dim-byte block:
+ *     K[16][head_dim]  token-major rows, then
+ *     V^T[head_dim][16] dimension-major (each row holds one dimension of the page's 16 tokens).
+ * Token slots >= length in a conversation's last page always hold zeros (append and unpack write
+ * them), so a page is never read past the conversation's end with undefined contents.
+ */
+size_t cs_pool_kv_bytes(const cs_pool_desc* desc);
+
+/* Device workspace bytes the pool needs (page-table mirror, decode partials, metadata ring). */
+size_t cs_pool_workspace_bytes(const cs_pool_desc* desc);
+
+/*
+ * Create a pool over caller memory. Physical pages are handed out from a free list shuffled by
+ * `placement_seed`, so page placement is random (results never depend on it). Pinned host staging
+ * memory for metadata uploads is allocated here and freed by cs_pool_destroy.
+ * Errors: CS_EINVAL (bad descriptor, null/short/misaligned buffers), CS_EHIP.
+ */
+cs_status cs_pool_create(const cs_pool_desc* desc, void* kv_base, size_t kv_bytes, void* ws_base,
+                         size_t ws_bytes, uint64_t placement_seed, cs_pool** out);
+
+/* Destroy host state; never frees caller memory. Waits for the pool's enqueued work first. */
+cs_status cs_pool_destroy(cs_pool* pool);
+
+/* Pages held by live conversations and pages still free (the decoder's active KV occupancy that
+ * the paper's reactive scheduler reads, Section 4.2; freed when a conversation ends). */
+cs_status cs_pool_occupancy(const cs_pool* pool, int64_t* used_pages, int64_t* free_pages);
+
+/* New empty conversation (Section 4.2: a conversation enters at its first turn).
+ * Errors: CS_EINVAL (null out), CS_ENOMEM (max_convs live). */
+cs_status cs_conv_create(cs_pool* pool, cs_conv* out);
+
+/* End a conversation and return its pages to the pool (Section 4.2: occupancy is decremented at
+ * termination). The caller must not destroy a conversation that enqueued work still reads.
+ * Errors: CS_ENOENT. */
+cs_status cs_conv_destroy(cs_pool* pool, cs_conv conv);
+
+/* Current length in tokens. Errors: CS_ENOENT, CS_EINVAL. */
+cs_status cs_conv_len(const cs_pool* pool, cs_conv conv, int64_t* tokens);
+
+/* Copy the conversation's physical page ids (logical order) into out[0..cap); *n = page count.
+ * Errors: CS_ENOENT, CS_EINVAL (null), CS_ERANGE (cap < page count; *n still set). */
+cs_status cs_conv_pages(const cs_pool* pool, cs_conv conv, int32_t* out, int64_t cap, int64_t* n);
+
+/*
+ * Append n_new tokens of K and V for every layer (Section 2.1: decode appends one KV entry per
+ * generated token; Section 3.1: a later turn adds the entries of its appended tokens).
+ * k, v: device, [n_layers][n_new][n_kv_heads][head_dim] bf16, contiguous.
+ * Reserves ceil((len+n_new)/16) - ceil(len/16) new pages first; on CS_ENOMEM nothing changes.
+ * n_new == 0 is a no-op. Errors: CS_ENOENT, CS_EINVAL, CS_ENOMEM, CS_ERANGE, CS_EHIP.
+ */
+cs_status cs_kv_append(cs_pool* pool, cs_conv conv, int32_t n_new, const void* k, const void* v,
+                       cs_stream stream);
+
+/*
+ * Batched append: conversation convs[i] receives n_new[i] tokens; k, v are
+ * [n_layers][sum(n_new)][n_kv_heads][head_dim] with the conversations' tokens concatenated in
+ * batch order. All-or-nothing page reservation. Conversations must be distinct.
+ */
+cs_status cs_kv_append_batch(cs_pool* pool, int32_t n_convs, const cs_conv* convs,
+                             const int32_t* n_new, const void* k, const void* v, cs_stream stream);
+
+/*
+ * Turn-1 causal prefill (Section 3.1: the compute-bound first-turn prefill). For each conversation
+ * q_lens[i] must equal its length (its whole content is the prompt just appended).
+ * q:   device [sum(q_lens)][n_q_heads][head_dim] bf16, conversations in batch order.
+ * out: device, same shape; bf16 (round to nearest even) of softmax(q k^T / sqrt(d)) v, causal.
+ * Errors: CS_EINVAL (null, duplicate conv, q_len < 0), CS_ENOENT, CS_ESTATE (q_len != length),
+ * CS_ERANGE (layer), CS_ENOMEM (metadata larger than the ring), CS_EHIP.
+ */
+cs_status cs_attn_prefill_turn1(cs_pool* pool, int32_t n_convs, const cs_conv* convs,
+                                const int32_t* q_lens, int32_t layer, const void* q, void* out,
+                                cs_stream stream);
+
+/*
+ * Extend-prefill of a later turn (Section 3.1 "prefix caching": the appended tokens attend to the
+ * whole cached history and causally among themselves; Section 4: it runs on the pinned decoder).
+ * Same arguments as cs_attn_prefill_turn1 but 0 <= q_lens[i] <= length (q_len == length is a full
+ * prefill, q_len == 1 a decode). Errors as above, CS_ESTATE when q_len > length.
+ */
+cs_status cs_attn_extend(cs_pool* pool, int32_t n_convs, const cs_conv* convs,
+                         const int32_t* q_lens, int32_t layer, const void* q, void* out,
+                         cs_stream stream);
+
+/*
+ * Batched single-token decode (Section 2.1 / 3.2: each step reads the whole cache of every
+ * conversation in the batch; memory-bound). The query of convs[i] is its last position.
+ * q, out: device [n_convs][n_q_heads][head_dim] bf16. Conversations distinct, length >= 1.
+ * Split-K over fixed logical token ranges plus a fixed-order log-sum-exp merge: the result is
+ * bitwise deterministic and independent of physical page placement.
+ * Errors: CS_EINVAL, CS_ENOENT, CS_ESTATE (length 0), CS_ERANGE, CS_ENOMEM, CS_EHIP.
+ */
+cs_status cs_attn_decode_batch(cs_pool* pool, int32_t n_convs, const cs_conv* convs,
+                               int32_t layer, const void* q, void* out, cs_stream stream);
+
+/* Wire size of a conversation's KV: n_layers * ceil(len/16) * n_kv_heads * 64 * head_dim bytes. */
+cs_status cs_kv_pack_size(const cs_pool* pool, cs_conv conv, size_t* bytes);
+
+/*
+ * Gather a conversation's pages in logical order into a contiguous wire buffer (the sending half
+ * of the one-time turn-1 KV transfer, Section 4 and Section 3.1 "KV cache transfer").
+ * Wire layout: [layer][logical page][kv_head] blocks in the pool's block format (K[16][d] then
+ * V^T[d][16]); token slots >= length are written as zeros. dst: device, dst_bytes must equal
+ * cs_kv_pack_size. Errors: CS_ENOENT, CS_EINVAL, CS_EHIP.
+ */
+cs_status cs_kv_pack(const cs_pool* pool, cs_conv conv, void* dst, size_t dst_bytes,
+                     cs_stream stream);
+
+/*
+ * Receiving half of the transfer: create a conversation of n_tokens tokens in `pool`, take fresh
+ * pages from its (randomly placed) free list and scatter the wire buffer into them. src_bytes must
+ * equal the wire size for n_tokens with this pool's shape; tail slots are written as zeros.
+ * Errors: CS_EINVAL (size mismatch, n_tokens < 1), CS_ENOMEM, CS_ERANGE, CS_EHIP.
+ */
+cs_status cs_kv_unpack(cs_pool* pool, const void* src, size_t src_bytes, int64_t n_tokens,
+                       cs_conv* out_conv, cs_stream stream);
+
+/* Message of the last failing call on this thread ("" if none). Valid until the next call. */
+const char* cs_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CONSERVE_ATTN_H */

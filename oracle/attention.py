@@ -2,7 +2,7 @@
 
 What it follows
 ---------------
-* Section 2.2 (LLM serving techniques): prefill produces a KV entry for every prompt token; a decode
+* Section 2.1 (LLM Serving Techniques): prefill produces a KV entry for every prompt token; a decode
   step reads the full KV cache and appends one new entry.
 * Section 3.1 (prefix caching paragraph) and Section 4 (design): a later turn computes KV only for
   its appended tokens and attends against the whole cached history of the conversation.

@@ -2,7 +2,7 @@
 
 What it follows
 ---------------
-* Section 1 and Section 2.2: a conversation's KV cache only grows; decode appends one entry per
+* Section 1 and Section 2.1: a conversation's KV cache only grows; decode appends one entry per
   generated token, and a later turn appends the entries of its new tokens (Section 3.1).
 * Section 4 (design) and Section 5.1: the turn-1 cache is produced on the prefiller and transferred
   exactly once to the decoder the conversation is bound to.

@@ -1,0 +1,279 @@
+// Turn-1 prefill and turn-N extend-prefill attention over paged KV (flash-attention forward).
+//
+// A workgroup owns one (conversation, 64-query block, kv head) tile; its G waves are the G query
+// heads of that kv head (the GQA group), so every K/V tile staged in LDS serves 64*G query rows.
+// Each wave computes the transposed score tile on the matrix cores (v_mfma_f32_32x32x16_bf16):
+//   S^T[key][query] = K[key][:] . Q[query][:]       A = K rows from LDS, B = Q kept in registers
+//   O^T[dim][query] += V^T[dim][key] . P^T[key][query]   A = V^T rows from LDS, B = P registers
+// With the transposed formulation every lane owns one query row (32 rows of a 32x32 tile, the
+// two 32-lane halves holding alternating groups of 4 keys), so the online-softmax max/sum are
+// in-lane except for one exchange between the halves, and the P accumulator registers are
+// directly the B operand of the PV product (the key order inside V^T is permuted in LDS to match).
+// K/V tiles of 64 keys (4 pages) are double-buffered in LDS; fully visible tiles skip the mask.
+#include <cmath>
+
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace cs {
+
+struct ExtendArgs {
+  const uint16_t* pool;
+  int64_t n_pages;
+  int n_kv_heads;
+  int layer;
+  const int32_t* page_table;
+  int max_pages;
+  const ExtendConvDesc* convs;
+  const ExtendTile* tiles;
+  const uint16_t* q;
+  uint16_t* out;
+  float scale_log2;
+};
+
+constexpr int kBN = 64;  // keys per tile
+constexpr int kBM = 64;  // query tokens per workgroup
+
+template <int D>
+struct FwdSmem {
+  static constexpr int kRowK = D + 8;    // K tile row stride (elements), padded
+  static constexpr int kRowV = kBN + 8;  // V^T tile row stride (elements), padded
+  uint16_t k[2][kBN][kRowK];
+  uint16_t v[2][D][kRowV];
+};
+
+// Position of key group c (4 keys) of a 16-key group inside the permuted V^T row:
+// groups hold keys {0-3, 8-11, 4-7, 12-15} so that 32-lane half h reads keys {4h..4h+3, 8+4h..}
+// as one 16-byte run.
+__device__ __forceinline__ int vt_group_pos(int c) { return ((c & 1) << 1) | (c >> 1); }
+
+template <int D, int G>
+__global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
+  constexpr int NT = 64 * G;           // threads
+  constexpr int KS = D / 16;           // k-steps of QK^T (16 dims each)
+  constexpr int DT = D / 32;           // 32-dim output tiles
+  constexpr int CH = kBN * D / 8;      // 16-byte chunks per K (or V^T) tile
+  constexpr int PER = CH / NT;         // chunks per thread per tile
+  static_assert(CH % NT == 0, "tile chunks must divide the workgroup");
+  __shared__ FwdSmem<D> sm;
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tile_idx = blockIdx.x / a.n_kv_heads, g = blockIdx.x % a.n_kv_heads;
+  const ExtendTile tile = a.tiles[tile_idx];
+  const ExtendConvDesc cd = a.convs[tile.conv];
+  const int prefix = cd.len - cd.q_len;
+  const int q_hi = min(cd.q_len, tile.q0 + kBM);             // queries [q0, q_hi)
+  const int pos_min = prefix + tile.q0, pos_max = prefix + q_hi - 1;
+  const int n_kt = pos_max / kBN + 1;                        // key tiles 0 .. n_kt-1
+  const int n_pg = (cd.len + kPageTokens - 1) / kPageTokens;
+  const int32_t* pt = a.page_table + static_cast<size_t>(cd.slot) * a.max_pages;
+  const int h = g * G + wave;                                 // query head of this wave
+  const int n_q_heads = a.n_kv_heads * G;
+  const size_t head_stride = static_cast<size_t>(2 * kPageTokens * D);
+  const size_t layer_base = static_cast<size_t>(a.layer) * a.n_pages * a.n_kv_heads * head_stride +
+                            static_cast<size_t>(g) * head_stride;
+  const size_t page_stride = static_cast<size_t>(a.n_kv_heads) * head_stride;
+
+  // ---- global -> register staging of one K/V tile (pages 4j .. 4j+3) ------------------------
+  uint4 kreg[PER], vreg[PER];
+  auto load_tile = [&](int j) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = tid + u * NT;
+      const int p = i / (2 * D);                 // page within tile (2D chunks per page)
+      const int lp = 4 * j + p;
+      kreg[u] = make_uint4(0, 0, 0, 0);
+      vreg[u] = make_uint4(0, 0, 0, 0);
+      if (lp < n_pg) {
+        const uint16_t* blk = a.pool + layer_base + static_cast<size_t>(pt[lp]) * page_stride;
+        const int w = i % (2 * D);
+        kreg[u] = ld16(blk + w * 8);                        // K: row w/(D/8), chunk w%(D/8)
+        vreg[u] = ld16(blk + kPageTokens * D + w * 8);      // V^T: dim w/2, keys 8*(w%2)..+8
+        const int key0 = kBN * j + kPageTokens * p + 8 * (w & 1);
+        if (key0 + 8 > cd.len) {                            // zero V of keys past the end
+          vreg[u].x = mask_bf16x2(vreg[u].x, key0 + 0 < cd.len, key0 + 1 < cd.len);
+          vreg[u].y = mask_bf16x2(vreg[u].y, key0 + 2 < cd.len, key0 + 3 < cd.len);
+          vreg[u].z = mask_bf16x2(vreg[u].z, key0 + 4 < cd.len, key0 + 5 < cd.len);
+          vreg[u].w = mask_bf16x2(vreg[u].w, key0 + 6 < cd.len, key0 + 7 < cd.len);
+        }
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = tid + u * NT;
+      const int p = i / (2 * D), w = i % (2 * D);
+      const int row = kPageTokens * p + w / (D / 8), col = (w % (D / 8)) * 8;
+      st16(&sm.k[buf][row][col], kreg[u]);
+      const int dim = w >> 1, c0 = 2 * (w & 1);             // key groups c0, c0+1 of the page
+      uint16_t* vrow = &sm.v[buf][dim][kPageTokens * p];
+      st8(vrow + 4 * vt_group_pos(c0), make_uint2(vreg[u].x, vreg[u].y));
+      st8(vrow + 4 * vt_group_pos(c0 + 1), make_uint2(vreg[u].z, vreg[u].w));
+    }
+  };
+
+  // ---- Q operand in registers: query q0 + 32*qt + lane%32, dims 16*ks + 8*(lane/32) ---------
+  const int half = lane >> 5, col = lane & 31;
+  bf16x8 qop[2][KS];
+  int qpos[2];
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    const int qi = tile.q0 + 32 * qt + col;
+    const bool valid = qi < cd.q_len;
+    qpos[qt] = prefix + (valid ? qi : cd.q_len - 1);
+    const uint16_t* qrow = a.q + (static_cast<size_t>(cd.q_row + (valid ? qi : 0)) * n_q_heads + h) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qop[qt][ks] = valid ? as_bf16x8(ld16(qrow + 16 * ks + 8 * half)) : bf16x8{};
+  }
+
+  f32x16 o[DT][2];
+#pragma unroll
+  for (int t = 0; t < DT; ++t)
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[t][qt][e] = 0.f;
+  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+
+  for (int j = 0; j < n_kt; ++j) {
+    const int buf = j & 1;
+    if (j + 1 < n_kt) load_tile(j + 1);
+
+    // S^T tiles: [key subtile kt2][query tile qt]
+    f32x16 s[2][2];
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s[kt2][qt][e] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int kt2 = 0; kt2 < 2; ++kt2) {
+        const bf16x8 kop = as_bf16x8(ld16(&sm.k[buf][32 * kt2 + col][16 * ks + 8 * half]));
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+          s[kt2][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[qt][ks], s[kt2][qt], 0, 0, 0);
+      }
+    }
+
+    // Online softmax per query (one per lane and query tile).
+    const bool need_mask = kBN * j + kBN - 1 > pos_min;
+    bf16x8 pop[2][2][2];  // [qt][kt2][j2]
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = kBN * j + 32 * kt2 + 8 * (e >> 2) + 4 * half + (e & 3);
+          float x = s[kt2][qt][e] * a.scale_log2;
+          if (need_mask && key > qpos[qt]) x = -INFINITY;
+          s[kt2][qt][e] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, xor_shfl(mx, 32));
+      const float m_new = fmaxf(m_run[qt], mx);
+      const float alpha = fast_exp2(m_run[qt] - m_new);
+      m_run[qt] = m_new;
+      float psum = 0.f;
+#pragma unroll
+      for (int kt2 = 0; kt2 < 2; ++kt2) {
+        float p[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) p[e] = fast_exp2(s[kt2][qt][e] - m_new);
+#pragma unroll
+        for (int j2 = 0; j2 < 2; ++j2) {
+          const uint4 pw = make_uint4(pack_bf16x2(p[8 * j2 + 0], p[8 * j2 + 1]),
+                                      pack_bf16x2(p[8 * j2 + 2], p[8 * j2 + 3]),
+                                      pack_bf16x2(p[8 * j2 + 4], p[8 * j2 + 5]),
+                                      pack_bf16x2(p[8 * j2 + 6], p[8 * j2 + 7]));
+          // the denominator sums the same bf16-rounded weights the PV product uses
+          psum += (sum_bf16x2(pw.x) + sum_bf16x2(pw.y)) + (sum_bf16x2(pw.z) + sum_bf16x2(pw.w));
+          pop[qt][kt2][j2] = __builtin_bit_cast(bf16x8, pw);
+        }
+      }
+      l_run[qt] = l_run[qt] * alpha + psum;
+#pragma unroll
+      for (int t = 0; t < DT; ++t) o[t][qt] *= alpha;
+    }
+
+    // O^T += V^T . P^T over the 4 k-steps (16 keys each) of the tile.
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+      for (int j2 = 0; j2 < 2; ++j2)
+#pragma unroll
+        for (int t = 0; t < DT; ++t) {
+          const bf16x8 vop =
+              as_bf16x8(ld16(&sm.v[buf][32 * t + col][32 * kt2 + 16 * j2 + 8 * half]));
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt)
+            o[t][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[qt][kt2][j2], o[t][qt], 0, 0, 0);
+        }
+
+    if (j + 1 < n_kt) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  // Normalise and write: lane owns query col of tile qt, dims 32t + 8(e/4) + 4*half + e%4.
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    const int qi = tile.q0 + 32 * qt + col;
+    const float l_tot = l_run[qt] + xor_shfl(l_run[qt], 32);
+    if (qi >= cd.q_len) continue;
+    const float inv = 1.f / l_tot;
+    uint16_t* orow = a.out + (static_cast<size_t>(cd.q_row + qi) * n_q_heads + h) * D;
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int dim = 32 * t + 8 * e4 + 4 * half;
+        st8(orow + dim, make_uint2(pack_bf16x2(o[t][qt][4 * e4 + 0] * inv, o[t][qt][4 * e4 + 1] * inv),
+                                   pack_bf16x2(o[t][qt][4 * e4 + 2] * inv, o[t][qt][4 * e4 + 3] * inv)));
+      }
+  }
+}
+
+template <int D, int G>
+static void launch_fwd(const ExtendArgs& a, int n_tiles, int n_kv_heads, hipStream_t stream) {
+  attn_fwd_kernel<D, G><<<n_tiles * n_kv_heads, 64 * G, 0, stream>>>(a);
+}
+
+hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,
+                         const ExtendTile* d_tiles, int n_tiles, const void* q, void* out,
+                         hipStream_t stream) {
+  if (n_tiles == 0) return hipSuccess;
+  ExtendArgs a;
+  a.pool = static_cast<const uint16_t*>(g.pool);
+  a.n_pages = g.n_pages;
+  a.n_kv_heads = g.n_kv_heads;
+  a.layer = layer;
+  a.page_table = g.page_table;
+  a.max_pages = g.max_pages;
+  a.convs = d_convs;
+  a.tiles = d_tiles;
+  a.q = static_cast<const uint16_t*>(q);
+  a.out = static_cast<uint16_t*>(out);
+  a.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(g.head_dim)));
+  const int G = g.n_q_heads / g.n_kv_heads;
+#define CS_FWD_CASE(DD, GG)                                   \
+  if (g.head_dim == DD && G == GG) {                          \
+    launch_fwd<DD, GG>(a, n_tiles, g.n_kv_heads, stream);     \
+    return hipGetLastError();                                 \
+  }
+  CS_FWD_CASE(128, 1) CS_FWD_CASE(128, 2) CS_FWD_CASE(128, 4) CS_FWD_CASE(128, 8)
+  CS_FWD_CASE(64, 1) CS_FWD_CASE(64, 2) CS_FWD_CASE(64, 4) CS_FWD_CASE(64, 8)
+#undef CS_FWD_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace cs

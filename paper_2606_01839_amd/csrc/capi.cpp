@@ -1,0 +1,535 @@
+// C ABI of the library (declared in include/conserve_attn.h): argument validation, host metadata
+// (pages, conversations, plans), metadata upload through a pinned ring, kernel launches.
+#include "conserve_attn.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <unordered_set>
+#include <vector>
+
+#include "host/host_state.hpp"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+cs_status fail(cs_status code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+constexpr size_t kAlign = 256;
+constexpr size_t kRingBytes = size_t(8) << 20;  // metadata ring (device + pinned host), 4 quarters
+constexpr size_t kQuarter = kRingBytes / 4;
+constexpr int kMinSplit = 128;                   // smallest decode split: bounds the partials
+constexpr int64_t kDecodeTargetItems = 4096;     // work items a decode launch aims for
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct WsLayout {
+  size_t page_table, partials, ring, total;
+  size_t partial_floats;
+};
+
+int64_t max_decode_items(const cs_pool_desc& d) {
+  // sum_b ceil(L_b / kMinSplit) <= total tokens / kMinSplit + batch
+  return d.n_pages * cs::kPage / kMinSplit + d.max_convs;
+}
+
+WsLayout ws_layout(const cs_pool_desc& d) {
+  WsLayout w{};
+  const int group = d.n_q_heads / d.n_kv_heads;
+  w.page_table = 0;
+  size_t pt_bytes = static_cast<size_t>(d.max_convs) * static_cast<size_t>(d.max_pages_per_conv) * 4;
+  w.partials = align_up(pt_bytes, kAlign);
+  w.partial_floats = static_cast<size_t>(max_decode_items(d)) * d.n_kv_heads * group * (d.head_dim + 2);
+  w.ring = align_up(w.partials + w.partial_floats * 4, kAlign);
+  w.total = w.ring + kRingBytes;
+  return w;
+}
+
+const char* desc_problem(const cs_pool_desc* d) {
+  if (!d) return "null descriptor";
+  if (d->n_layers < 1) return "n_layers must be >= 1";
+  if (d->n_kv_heads < 1 || d->n_q_heads < 1 || d->n_q_heads % d->n_kv_heads != 0)
+    return "n_q_heads must be a positive multiple of n_kv_heads";
+  const int group = d->n_q_heads / d->n_kv_heads;
+  if (d->head_dim != 64 && d->head_dim != 128) return "head_dim must be 64 or 128";
+  if (d->head_dim == 128 && group != 2 && group != 4)
+    return "head_dim 128 supports n_q_heads/n_kv_heads in {2, 4}";
+  if (d->head_dim == 64 && group != 1 && group != 2 && group != 4 && group != 8)
+    return "head_dim 64 supports n_q_heads/n_kv_heads in {1, 2, 4, 8}";
+  if (d->max_convs < 1 || d->max_convs > (1 << cs::ConvTable::kSlotBits))
+    return "max_convs must be in [1, 2^20]";
+  if (d->max_pages_per_conv < 1 || d->max_pages_per_conv > (1 << 26))
+    return "max_pages_per_conv must be in [1, 2^26]";
+  if (d->n_pages < 1 || d->n_pages > INT32_MAX) return "n_pages must be in [1, 2^31)";
+  return nullptr;
+}
+
+}  // namespace
+
+struct cs_pool {
+  cs_pool_desc desc;
+  char* kv;
+  size_t kv_bytes;
+  char* ws;
+  size_t ws_bytes;
+  WsLayout lay;
+  cs::PagePool pages;
+  cs::ConvTable convs;
+  // device resources, created on first use
+  bool dev_ready = false;
+  int device = -1;
+  char* h_ring = nullptr;
+  size_t ring_head = 0;
+  int cur_quarter = -1;
+  hipEvent_t quarter_ev[4] = {};
+  bool quarter_used[4] = {};
+  hipEvent_t switch_ev = nullptr;
+  hipStream_t stream = nullptr;
+  bool have_stream = false;
+
+  cs_pool(const cs_pool_desc& d, char* kvp, size_t kvb, char* wsp, size_t wsb, uint64_t seed)
+      : desc(d), kv(kvp), kv_bytes(kvb), ws(wsp), ws_bytes(wsb), lay(ws_layout(d)),
+        pages(d.n_pages, seed), convs(d.max_convs, d.max_pages_per_conv) {}
+
+  cs::PoolGeom geom() const {
+    cs::PoolGeom g;
+    g.pool = kv;
+    g.n_pages = desc.n_pages;
+    g.n_layers = desc.n_layers;
+    g.n_kv_heads = desc.n_kv_heads;
+    g.n_q_heads = desc.n_q_heads;
+    g.head_dim = desc.head_dim;
+    g.page_table = reinterpret_cast<int32_t*>(ws + lay.page_table);
+    g.max_pages = desc.max_pages_per_conv;
+    return g;
+  }
+  float* partials() const { return reinterpret_cast<float*>(ws + lay.partials); }
+};
+
+namespace {
+
+cs_status hip_fail(hipError_t e, const char* what) {
+  return fail(CS_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define CS_HIP(call, what)                        \
+  do {                                            \
+    hipError_t e_ = (call);                       \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+cs_status ensure_device(cs_pool* p) {
+  if (p->dev_ready) return CS_OK;
+  int dev = 0;
+  CS_HIP(hipGetDevice(&dev), "hipGetDevice");
+  void* h = nullptr;
+  CS_HIP(hipHostMalloc(&h, kRingBytes, hipHostMallocDefault), "hipHostMalloc(metadata ring)");
+  for (int i = 0; i < 4; ++i) {
+    hipError_t e = hipEventCreateWithFlags(&p->quarter_ev[i], hipEventDisableTiming);
+    if (e != hipSuccess) {
+      for (int k = 0; k < i; ++k) (void)hipEventDestroy(p->quarter_ev[k]);
+      (void)hipHostFree(h);
+      return hip_fail(e, "hipEventCreate");
+    }
+  }
+  hipError_t e = hipEventCreateWithFlags(&p->switch_ev, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    for (int k = 0; k < 4; ++k) (void)hipEventDestroy(p->quarter_ev[k]);
+    (void)hipHostFree(h);
+    return hip_fail(e, "hipEventCreate");
+  }
+  p->h_ring = static_cast<char*>(h);
+  p->device = dev;
+  p->dev_ready = true;
+  return CS_OK;
+}
+
+// All of a pool's work is chained on one stream at a time; a new stream first waits for the old.
+cs_status use_stream(cs_pool* p, hipStream_t s) {
+  if (p->have_stream && s != p->stream) {
+    CS_HIP(hipEventRecord(p->switch_ev, p->stream), "hipEventRecord");
+    CS_HIP(hipStreamWaitEvent(s, p->switch_ev, 0), "hipStreamWaitEvent");
+  }
+  p->stream = s;
+  p->have_stream = true;
+  return CS_OK;
+}
+
+// Reserve `n` bytes of the metadata ring inside one quarter. Entering a quarter records an event
+// closing the previous one (everything enqueued so far) and waits for the event that closed the
+// entered quarter last time round, so a region is never rewritten while a copy or kernel of an
+// earlier call may still read it.
+cs_status ring_reserve(cs_pool* p, size_t n, size_t* off_out) {
+  n = align_up(std::max<size_t>(n, 1), kAlign);
+  if (n > kQuarter) return fail(CS_ENOMEM, "metadata for one launch exceeds the upload ring");
+  size_t off = p->ring_head;
+  if (off / kQuarter != (off + n - 1) / kQuarter || off + n > kRingBytes)
+    off = ((off + kQuarter - 1) / kQuarter) * kQuarter;
+  if (off + n > kRingBytes) off = 0;
+  const int q = static_cast<int>(off / kQuarter);
+  if (q != p->cur_quarter) {
+    if (p->cur_quarter >= 0) {
+      CS_HIP(hipEventRecord(p->quarter_ev[p->cur_quarter], p->stream), "hipEventRecord");
+      p->quarter_used[p->cur_quarter] = true;
+    }
+    if (p->quarter_used[q]) CS_HIP(hipEventSynchronize(p->quarter_ev[q]), "hipEventSynchronize");
+    p->cur_quarter = q;
+  }
+  p->ring_head = off + n;
+  *off_out = off;
+  return CS_OK;
+}
+
+// Copy host bytes into the ring and enqueue their upload; returns the device address.
+cs_status upload(cs_pool* p, const void* src, size_t n, void** dev_out) {
+  size_t off = 0;
+  cs_status st = ring_reserve(p, n, &off);
+  if (st != CS_OK) return st;
+  std::memcpy(p->h_ring + off, src, n);
+  char* d = p->ws + p->lay.ring + off;
+  CS_HIP(hipMemcpyAsync(d, p->h_ring + off, n, hipMemcpyHostToDevice, p->stream), "hipMemcpyAsync");
+  *dev_out = d;
+  return CS_OK;
+}
+
+// Two host arrays uploaded back to back in one reservation.
+template <typename A, typename B>
+cs_status upload2(cs_pool* p, const std::vector<A>& a, const std::vector<B>& b, A** da, B** db) {
+  const size_t na = align_up(a.size() * sizeof(A), 16), nb = b.size() * sizeof(B);
+  size_t off = 0;
+  cs_status st = ring_reserve(p, na + nb, &off);
+  if (st != CS_OK) return st;
+  if (!a.empty()) std::memcpy(p->h_ring + off, a.data(), a.size() * sizeof(A));
+  if (!b.empty()) std::memcpy(p->h_ring + off + na, b.data(), nb);
+  char* d = p->ws + p->lay.ring + off;
+  CS_HIP(hipMemcpyAsync(d, p->h_ring + off, na + nb, hipMemcpyHostToDevice, p->stream),
+         "hipMemcpyAsync");
+  *da = reinterpret_cast<A*>(d);
+  *db = reinterpret_cast<B*>(d + na);
+  return CS_OK;
+}
+
+cs_status check_convs(const cs_pool* p, int32_t n, const cs_conv* convs, std::vector<const cs::Conv*>& out) {
+  if (n < 0) return fail(CS_EINVAL, "negative batch size");
+  if (n > 0 && !convs) return fail(CS_EINVAL, "null conversation array");
+  out.clear();
+  std::unordered_set<int32_t> seen;
+  for (int32_t i = 0; i < n; ++i) {
+    const cs::Conv* c = p->convs.find(convs[i]);
+    if (!c) return fail(CS_ENOENT, "unknown conversation handle " + std::to_string(convs[i]));
+    if (!seen.insert(convs[i]).second)
+      return fail(CS_EINVAL, "conversation " + std::to_string(convs[i]) + " appears twice in a batch");
+    out.push_back(c);
+  }
+  return CS_OK;
+}
+
+size_t wire_size(const cs_pool_desc& d, int64_t len) {
+  return static_cast<size_t>(d.n_layers) * static_cast<size_t>(cs::pages_for(len)) *
+         static_cast<size_t>(d.n_kv_heads) * 2 * cs::kPage * static_cast<size_t>(d.head_dim) * 2;
+}
+
+hipStream_t as_stream(cs_stream s) { return reinterpret_cast<hipStream_t>(s); }
+
+cs_status attend(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* q_lens, int32_t layer,
+                 const void* q, void* out, cs_stream stream, bool turn1) {
+  if (!p) return fail(CS_EINVAL, "null pool");
+  std::vector<const cs::Conv*> cv;
+  cs_status st = check_convs(p, n, convs, cv);
+  if (st != CS_OK) return st;
+  if (n > 0 && !q_lens) return fail(CS_EINVAL, "null q_lens");
+  if (layer < 0 || layer >= p->desc.n_layers) return fail(CS_ERANGE, "layer out of range");
+  int64_t rows = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (q_lens[i] < 0) return fail(CS_EINVAL, "negative q_len");
+    if (q_lens[i] > cv[i]->len)
+      return fail(CS_ESTATE, "q_len " + std::to_string(q_lens[i]) + " exceeds conversation length " +
+                                 std::to_string(cv[i]->len));
+    if (turn1 && q_lens[i] != cv[i]->len)
+      return fail(CS_ESTATE, "turn-1 prefill needs q_len == conversation length (append the prompt first)");
+    rows += q_lens[i];
+  }
+  if (rows == 0) return CS_OK;
+  if (rows > INT32_MAX) return fail(CS_EINVAL, "too many query rows");
+  if (!q || !out) return fail(CS_EINVAL, "null q/out");
+  if ((st = ensure_device(p)) != CS_OK) return st;
+  if ((st = use_stream(p, as_stream(stream))) != CS_OK) return st;
+
+  std::vector<int32_t> slots(n), ql(q_lens, q_lens + n);
+  std::vector<int64_t> lens(n);
+  for (int32_t i = 0; i < n; ++i) {
+    slots[i] = cs::ConvTable::slot_of(convs[i]);
+    lens[i] = cv[i]->len;
+  }
+  cs::ExtendPlan plan = cs::plan_extend(slots, lens, ql, 64);
+  const size_t max_tiles =
+      (kQuarter - align_up(plan.convs.size() * sizeof(cs::ExtendConvDesc), 16) - kAlign) /
+      sizeof(cs::ExtendTile);
+  const cs::PoolGeom g = p->geom();
+  for (size_t t0 = 0; t0 < plan.tiles.size(); t0 += max_tiles) {
+    const size_t t1 = std::min(plan.tiles.size(), t0 + max_tiles);
+    std::vector<cs::ExtendTile> part(plan.tiles.begin() + t0, plan.tiles.begin() + t1);
+    cs::ExtendConvDesc* dc = nullptr;
+    cs::ExtendTile* dt = nullptr;
+    if ((st = upload2(p, plan.convs, part, &dc, &dt)) != CS_OK) return st;
+    CS_HIP(cs::launch_extend(g, layer, dc, dt, static_cast<int>(part.size()), q, out, p->stream),
+           "attention launch");
+  }
+  return CS_OK;
+}
+
+cs_status append_impl(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* n_new,
+                      const void* k, const void* v, cs_stream stream) {
+  if (!p) return fail(CS_EINVAL, "null pool");
+  std::vector<const cs::Conv*> cv;
+  cs_status st = check_convs(p, n, convs, cv);
+  if (st != CS_OK) return st;
+  if (n > 0 && !n_new) return fail(CS_EINVAL, "null n_new");
+  int64_t total = 0, need_pages = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (n_new[i] < 0) return fail(CS_EINVAL, "negative token count");
+    const int64_t nl = cv[i]->len + n_new[i];
+    if (cs::pages_for(nl) > p->desc.max_pages_per_conv)
+      return fail(CS_ERANGE, "conversation would exceed max_pages_per_conv");
+    need_pages += cs::pages_for(nl) - cs::pages_for(cv[i]->len);
+    total += n_new[i];
+  }
+  if (total == 0) return CS_OK;
+  if (total > INT32_MAX) return fail(CS_EINVAL, "too many tokens in one append");
+  if (!k || !v) return fail(CS_EINVAL, "null k/v");
+  if (need_pages > p->pages.free_count())
+    return fail(CS_ENOMEM, "KV pool exhausted: need " + std::to_string(need_pages) + " pages, " +
+                               std::to_string(p->pages.free_count()) + " free");
+  if ((st = ensure_device(p)) != CS_OK) return st;
+  if ((st = use_stream(p, as_stream(stream))) != CS_OK) return st;
+
+  // Commit host metadata: reserve pages (cannot fail now), build chunks, update lengths.
+  std::vector<int32_t> slots(n), nn(n_new, n_new + n);
+  std::vector<int64_t> old_lens(n);
+  std::vector<const std::vector<int32_t>*> lists(n);
+  for (int32_t i = 0; i < n; ++i) {
+    cs::Conv* c = p->convs.find(convs[i]);
+    slots[i] = cs::ConvTable::slot_of(convs[i]);
+    old_lens[i] = c->len;
+    p->pages.alloc(cs::pages_for(c->len + n_new[i]) - cs::pages_for(c->len), c->pages);
+    lists[i] = &c->pages;
+  }
+  std::vector<cs::PageChunk> chunks = cs::plan_append(slots, old_lens, nn, lists);
+  for (int32_t i = 0; i < n; ++i) p->convs.find(convs[i])->len += n_new[i];
+
+  const cs::PoolGeom g = p->geom();
+  const size_t per = kQuarter / sizeof(cs::PageChunk) - 1;
+  for (size_t c0 = 0; c0 < chunks.size(); c0 += per) {
+    const size_t c1 = std::min(chunks.size(), c0 + per);
+    void* d = nullptr;
+    if ((st = upload(p, chunks.data() + c0, (c1 - c0) * sizeof(cs::PageChunk), &d)) != CS_OK) return st;
+    CS_HIP(cs::launch_append(g, static_cast<const cs::PageChunk*>(d), static_cast<int>(c1 - c0), k, v,
+                             total, p->stream),
+           "append launch");
+  }
+  return CS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* cs_last_error(void) { return g_err.c_str(); }
+
+size_t cs_pool_kv_bytes(const cs_pool_desc* d) {
+  if (desc_problem(d)) return 0;
+  return static_cast<size_t>(d->n_layers) * static_cast<size_t>(d->n_pages) *
+         static_cast<size_t>(d->n_kv_heads) * 2 * cs::kPage * static_cast<size_t>(d->head_dim) * 2;
+}
+
+size_t cs_pool_workspace_bytes(const cs_pool_desc* d) {
+  if (desc_problem(d)) return 0;
+  return ws_layout(*d).total;
+}
+
+cs_status cs_pool_create(const cs_pool_desc* d, void* kv_base, size_t kv_bytes, void* ws_base,
+                         size_t ws_bytes, uint64_t seed, cs_pool** out) {
+  if (const char* why = desc_problem(d)) return fail(CS_EINVAL, why);
+  if (!out) return fail(CS_EINVAL, "null out");
+  if (!kv_base || !ws_base) return fail(CS_EINVAL, "null kv or workspace base");
+  if (reinterpret_cast<uintptr_t>(kv_base) % kAlign || reinterpret_cast<uintptr_t>(ws_base) % kAlign)
+    return fail(CS_EINVAL, "kv and workspace bases must be 256-byte aligned");
+  if (kv_bytes < cs_pool_kv_bytes(d)) return fail(CS_EINVAL, "kv buffer smaller than cs_pool_kv_bytes");
+  if (ws_bytes < cs_pool_workspace_bytes(d))
+    return fail(CS_EINVAL, "workspace smaller than cs_pool_workspace_bytes");
+  cs_pool* p = new (std::nothrow)
+      cs_pool(*d, static_cast<char*>(kv_base), kv_bytes, static_cast<char*>(ws_base), ws_bytes, seed);
+  if (!p) return fail(CS_ENOMEM, "host allocation failed");
+  *out = p;
+  return CS_OK;
+}
+
+cs_status cs_pool_destroy(cs_pool* p) {
+  if (!p) return fail(CS_EINVAL, "null pool");
+  cs_status st = CS_OK;
+  if (p->dev_ready) {
+    if (p->have_stream && hipStreamSynchronize(p->stream) != hipSuccess)
+      st = fail(CS_EHIP, "hipStreamSynchronize failed while destroying the pool");
+    for (auto& e : p->quarter_ev) (void)hipEventDestroy(e);
+    (void)hipEventDestroy(p->switch_ev);
+    (void)hipHostFree(p->h_ring);
+  }
+  delete p;
+  return st;
+}
+
+cs_status cs_pool_occupancy(const cs_pool* p, int64_t* used, int64_t* free_pages) {
+  if (!p || !used || !free_pages) return fail(CS_EINVAL, "null argument");
+  *used = p->pages.used_count();
+  *free_pages = p->pages.free_count();
+  return CS_OK;
+}
+
+cs_status cs_conv_create(cs_pool* p, cs_conv* out) {
+  if (!p || !out) return fail(CS_EINVAL, "null argument");
+  if (!p->convs.create(out)) return fail(CS_ENOMEM, "all conversation slots are live");
+  return CS_OK;
+}
+
+cs_status cs_conv_destroy(cs_pool* p, cs_conv conv) {
+  if (!p) return fail(CS_EINVAL, "null pool");
+  if (!p->convs.find(conv)) return fail(CS_ENOENT, "unknown conversation handle");
+  p->convs.destroy(conv, p->pages);
+  return CS_OK;
+}
+
+cs_status cs_conv_len(const cs_pool* p, cs_conv conv, int64_t* tokens) {
+  if (!p || !tokens) return fail(CS_EINVAL, "null argument");
+  const cs::Conv* c = p->convs.find(conv);
+  if (!c) return fail(CS_ENOENT, "unknown conversation handle");
+  *tokens = c->len;
+  return CS_OK;
+}
+
+cs_status cs_conv_pages(const cs_pool* p, cs_conv conv, int32_t* out, int64_t cap, int64_t* n) {
+  if (!p || !n) return fail(CS_EINVAL, "null argument");
+  const cs::Conv* c = p->convs.find(conv);
+  if (!c) return fail(CS_ENOENT, "unknown conversation handle");
+  *n = static_cast<int64_t>(c->pages.size());
+  if (cap < *n) return fail(CS_ERANGE, "output capacity smaller than the page count");
+  if (*n > 0 && !out) return fail(CS_EINVAL, "null output");
+  std::copy(c->pages.begin(), c->pages.end(), out);
+  return CS_OK;
+}
+
+cs_status cs_kv_append(cs_pool* p, cs_conv conv, int32_t n_new, const void* k, const void* v,
+                       cs_stream stream) {
+  return append_impl(p, 1, &conv, &n_new, k, v, stream);
+}
+
+cs_status cs_kv_append_batch(cs_pool* p, int32_t n_convs, const cs_conv* convs, const int32_t* n_new,
+                             const void* k, const void* v, cs_stream stream) {
+  return append_impl(p, n_convs, convs, n_new, k, v, stream);
+}
+
+cs_status cs_attn_prefill_turn1(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* q_lens,
+                                int32_t layer, const void* q, void* out, cs_stream stream) {
+  return attend(p, n, convs, q_lens, layer, q, out, stream, true);
+}
+
+cs_status cs_attn_extend(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* q_lens,
+                         int32_t layer, const void* q, void* out, cs_stream stream) {
+  return attend(p, n, convs, q_lens, layer, q, out, stream, false);
+}
+
+cs_status cs_attn_decode_batch(cs_pool* p, int32_t n, const cs_conv* convs, int32_t layer,
+                               const void* q, void* out, cs_stream stream) {
+  if (!p) return fail(CS_EINVAL, "null pool");
+  std::vector<const cs::Conv*> cv;
+  cs_status st = check_convs(p, n, convs, cv);
+  if (st != CS_OK) return st;
+  if (layer < 0 || layer >= p->desc.n_layers) return fail(CS_ERANGE, "layer out of range");
+  for (int32_t i = 0; i < n; ++i)
+    if (cv[i]->len < 1) return fail(CS_ESTATE, "decode on an empty conversation");
+  if (n == 0) return CS_OK;
+  if (!q || !out) return fail(CS_EINVAL, "null q/out");
+  if ((st = ensure_device(p)) != CS_OK) return st;
+  if ((st = use_stream(p, as_stream(stream))) != CS_OK) return st;
+  std::vector<int32_t> slots(n);
+  std::vector<int64_t> lens(n);
+  for (int32_t i = 0; i < n; ++i) {
+    slots[i] = cs::ConvTable::slot_of(convs[i]);
+    lens[i] = cv[i]->len;
+  }
+  cs::DecodePlan plan = cs::plan_decode(slots, lens, p->desc.n_kv_heads, kDecodeTargetItems);
+  if (plan.n_items > max_decode_items(p->desc))
+    return fail(CS_ENOMEM, "decode partials exceed the workspace");
+  void* d = nullptr;
+  if ((st = upload(p, plan.convs.data(), plan.convs.size() * sizeof(cs::DecodeConvDesc), &d)) != CS_OK)
+    return st;
+  CS_HIP(cs::launch_decode(p->geom(), layer, static_cast<const cs::DecodeConvDesc*>(d), n, plan.n_items,
+                           plan.split_tokens, q, out, p->partials(), p->stream),
+         "decode launch");
+  return CS_OK;
+}
+
+cs_status cs_kv_pack_size(const cs_pool* p, cs_conv conv, size_t* bytes) {
+  if (!p || !bytes) return fail(CS_EINVAL, "null argument");
+  const cs::Conv* c = p->convs.find(conv);
+  if (!c) return fail(CS_ENOENT, "unknown conversation handle");
+  *bytes = wire_size(p->desc, c->len);
+  return CS_OK;
+}
+
+cs_status cs_kv_pack(const cs_pool* pc, cs_conv conv, void* dst, size_t dst_bytes, cs_stream stream) {
+  cs_pool* p = const_cast<cs_pool*>(pc);  // host metadata is unchanged; stream/ring state is not
+  if (!p) return fail(CS_EINVAL, "null pool");
+  const cs::Conv* c = p->convs.find(conv);
+  if (!c) return fail(CS_ENOENT, "unknown conversation handle");
+  if (dst_bytes != wire_size(p->desc, c->len)) return fail(CS_EINVAL, "dst_bytes != cs_kv_pack_size");
+  if (c->len == 0) return CS_OK;
+  if (!dst) return fail(CS_EINVAL, "null dst");
+  cs_status st;
+  if ((st = ensure_device(p)) != CS_OK) return st;
+  if ((st = use_stream(p, as_stream(stream))) != CS_OK) return st;
+  CS_HIP(cs::launch_pack(p->geom(), cs::ConvTable::slot_of(conv), c->len, dst, p->stream), "pack launch");
+  return CS_OK;
+}
+
+cs_status cs_kv_unpack(cs_pool* p, const void* src, size_t src_bytes, int64_t n_tokens,
+                       cs_conv* out_conv, cs_stream stream) {
+  if (!p || !out_conv) return fail(CS_EINVAL, "null argument");
+  if (n_tokens < 1) return fail(CS_EINVAL, "n_tokens must be >= 1");
+  if (!src) return fail(CS_EINVAL, "null src");
+  const int64_t np = cs::pages_for(n_tokens);
+  if (np > p->desc.max_pages_per_conv) return fail(CS_ERANGE, "conversation exceeds max_pages_per_conv");
+  if (src_bytes != wire_size(p->desc, n_tokens))
+    return fail(CS_EINVAL, "src_bytes does not match the wire size of n_tokens for this pool");
+  if (p->convs.live_count() >= p->convs.max_convs()) return fail(CS_ENOMEM, "all conversation slots are live");
+  if (np > p->pages.free_count()) return fail(CS_ENOMEM, "KV pool exhausted");
+  cs_status st;
+  if ((st = ensure_device(p)) != CS_OK) return st;
+  if ((st = use_stream(p, as_stream(stream))) != CS_OK) return st;
+  cs_conv h;
+  p->convs.create(&h);
+  cs::Conv* c = p->convs.find(h);
+  p->pages.alloc(np, c->pages);
+  c->len = n_tokens;
+  *out_conv = h;
+  const size_t per = kQuarter / sizeof(int32_t) - 64;
+  for (size_t p0 = 0; p0 < c->pages.size(); p0 += per) {
+    const size_t p1 = std::min(c->pages.size(), p0 + per);
+    void* d = nullptr;
+    if ((st = upload(p, c->pages.data() + p0, (p1 - p0) * sizeof(int32_t), &d)) != CS_OK) return st;
+    CS_HIP(cs::launch_unpack(p->geom(), src, static_cast<const int32_t*>(d), cs::ConvTable::slot_of(h),
+                             n_tokens, static_cast<int>(p0), static_cast<int>(p1 - p0), p->stream),
+           "unpack launch");
+  }
+  return CS_OK;
+}
+
+}  // extern "C"

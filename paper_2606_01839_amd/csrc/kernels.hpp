@@ -1,0 +1,43 @@
+// Host-callable launchers of the gfx950 kernels (defined in the .hip files).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "host/host_state.hpp"
+
+namespace cs {
+
+struct PoolGeom {
+  void* pool;          // device base of the KV pool
+  int64_t n_pages;
+  int n_layers;
+  int n_kv_heads;
+  int n_q_heads;
+  int head_dim;
+  int32_t* page_table;  // device mirror [max_convs][max_pages]
+  int max_pages;
+};
+
+// KV append / unpack: write chunks (see PageChunk) of k,v [n_layers][src_rows][Hkv][D].
+hipError_t launch_append(const PoolGeom& g, const PageChunk* d_chunks, int n_chunks, const void* k,
+                         const void* v, int64_t src_rows, hipStream_t stream);
+
+// Pack: conversation pages (page-table row `slot`) -> wire [layer][lpage][head] blocks.
+hipError_t launch_pack(const PoolGeom& g, int slot, int64_t len, void* wire, hipStream_t stream);
+
+// Unpack: wire logical pages [lp0, lp0 + n_lp) -> physical pages d_pages[0..n_lp) of the
+// conversation in page-table row `slot` (length len).
+hipError_t launch_unpack(const PoolGeom& g, const void* wire, const int32_t* d_pages, int slot,
+                         int64_t len, int lp0, int n_lp, hipStream_t stream);
+
+// Decode: split kernel over plan items, then merge.
+hipError_t launch_decode(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs, int n_convs,
+                         int n_items, int split_tokens, const void* q, void* out, float* partials,
+                         hipStream_t stream);
+
+// Extend / prefill: one workgroup per (tile, kv head).
+hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,
+                         const ExtendTile* d_tiles, int n_tiles, const void* q, void* out,
+                         hipStream_t stream);
+
+}  // namespace cs

@@ -1,0 +1,193 @@
+// KV movement kernels: append new tokens into pages, pack a conversation into the transfer wire
+// format, unpack a wire buffer into freshly placed pages. Pure byte movement (bit-exact); every
+// one is HBM-bound. A pool block (layer, page, kv head) is K[16][D] token-major followed by
+// V^T[D][16] dimension-major; token slots past a conversation's end are kept zero.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace cs {
+
+// ---------------------------------------------------------------------------------------------
+// Append: one wave per (page chunk, layer, kv head). K rows are copied with 16-byte accesses;
+// V rows are staged in LDS and written transposed. Slots [t1, 16) of the chunk's page are zeroed.
+// ---------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(64) void kv_append_kernel(const PageChunk* __restrict__ chunks,
+                                                       const uint16_t* __restrict__ k_src,
+                                                       const uint16_t* __restrict__ v_src,
+                                                       int64_t src_rows, uint16_t* __restrict__ pool,
+                                                       int64_t n_pages, int n_kv_heads,
+                                                       int32_t* __restrict__ page_table,
+                                                       int max_pages) {
+  constexpr int kChunksPerRow = D / 8;            // 16-byte chunks per token row
+  constexpr int kRowsPerPass = 64 / kChunksPerRow;
+  __shared__ uint16_t vt[kPageTokens][D + 8];
+
+  const PageChunk c = chunks[blockIdx.x];
+  const int layer = blockIdx.y / n_kv_heads;
+  const int head = blockIdx.y % n_kv_heads;
+  const int lane = threadIdx.x;
+  uint16_t* blk = pool + block_elem<D>(layer, c.page, head, n_pages, n_kv_heads);
+
+  const int ch = lane % kChunksPerRow;
+#pragma unroll
+  for (int t = lane / kChunksPerRow; t < kPageTokens; t += kRowsPerPass) {
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    if (t >= c.t0 && t < c.t1) {
+      const size_t row = static_cast<size_t>(c.src_row) + static_cast<size_t>(t - c.t0);
+      const size_t src =
+          ((static_cast<size_t>(layer) * static_cast<size_t>(src_rows) + row) * n_kv_heads + head) *
+              D + ch * 8;
+      kv = ld16(k_src + src);
+      vv = ld16(v_src + src);
+    }
+    if (t >= c.t0) st16(blk + t * D + ch * 8, kv);
+    *reinterpret_cast<uint4*>(&vt[t][ch * 8]) = vv;
+  }
+  __syncthreads();
+
+  uint16_t* vdst = blk + kPageTokens * D;
+#pragma unroll
+  for (int e = lane; e < D; e += 64) {
+    uint16_t* row = vdst + e * kPageTokens;
+    if (c.t0 == 0) {
+      uint32_t w[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        w[j] = static_cast<uint32_t>(vt[2 * j][e]) | (static_cast<uint32_t>(vt[2 * j + 1][e]) << 16);
+      st16(row, make_uint4(w[0], w[1], w[2], w[3]));
+      st16(row + 8, make_uint4(w[4], w[5], w[6], w[7]));
+    } else {
+      for (int t = c.t0; t < kPageTokens; ++t) row[t] = vt[t][e];
+    }
+  }
+  if (c.new_page && blockIdx.y == 0 && lane == 0)
+    page_table[static_cast<size_t>(c.slot) * max_pages + c.lpage] = c.page;
+}
+
+// Zero the token slots >= valid inside 16-byte chunk i (8 elements) of a block.
+template <int D>
+__device__ __forceinline__ uint4 mask_tail(uint4 x, int i, int valid) {
+  const int e0 = 8 * i;
+  if (e0 < kPageTokens * D) {           // K part: chunk lies in token row e0 / D
+    return (e0 / D) < valid ? x : make_uint4(0, 0, 0, 0);
+  }
+  const int t0 = (e0 - kPageTokens * D) % kPageTokens;  // V^T part: tokens t0 .. t0+7 of one dim
+  x.x = mask_bf16x2(x.x, t0 + 0 < valid, t0 + 1 < valid);
+  x.y = mask_bf16x2(x.y, t0 + 2 < valid, t0 + 3 < valid);
+  x.z = mask_bf16x2(x.z, t0 + 4 < valid, t0 + 5 < valid);
+  x.w = mask_bf16x2(x.w, t0 + 6 < valid, t0 + 7 < valid);
+  return x;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Pack: one wave per (logical page, layer, kv head) block; all of a lane's loads are issued
+// before its stores. Tail slots of the last page are written as zeros.
+// ---------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(64) void kv_pack_kernel(const uint16_t* __restrict__ pool,
+                                                     int64_t n_pages, int n_kv_heads,
+                                                     const int32_t* __restrict__ pt_row, int64_t len,
+                                                     uint16_t* __restrict__ wire, int n_lpages) {
+  constexpr int kChunks = 2 * kPageTokens * D / 8;  // 16-byte chunks per block
+  constexpr int kPerLane = kChunks / 64;
+  const int lp = blockIdx.x;
+  const int layer = blockIdx.y / n_kv_heads, head = blockIdx.y % n_kv_heads;
+  const int page = pt_row[lp];
+  const uint16_t* src = pool + block_elem<D>(layer, page, head, n_pages, n_kv_heads);
+  uint16_t* dst = wire + ((static_cast<size_t>(layer) * n_lpages + lp) * n_kv_heads + head) *
+                             static_cast<size_t>(2 * kPageTokens * D);
+  const int64_t rem = len - static_cast<int64_t>(lp) * kPageTokens;
+  const int valid = rem < kPageTokens ? static_cast<int>(rem) : kPageTokens;
+  uint4 x[kPerLane];
+#pragma unroll
+  for (int j = 0; j < kPerLane; ++j) x[j] = ld16(src + 8 * (threadIdx.x + 64 * j));
+#pragma unroll
+  for (int j = 0; j < kPerLane; ++j) {
+    const int i = threadIdx.x + 64 * j;
+    st16(dst + 8 * i, valid < kPageTokens ? mask_tail<D>(x[j], i, valid) : x[j]);
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Unpack: inverse of pack into pages d_pages[lp]; also fills the page-table mirror row.
+// ---------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(64) void kv_unpack_kernel(const uint16_t* __restrict__ wire,
+                                                       const int32_t* __restrict__ d_pages,
+                                                       int64_t len, uint16_t* __restrict__ pool,
+                                                       int64_t n_pages, int n_kv_heads,
+                                                       int32_t* __restrict__ pt_row, int n_lpages,
+                                                       int lp0) {
+  constexpr int kChunks = 2 * kPageTokens * D / 8;
+  constexpr int kPerLane = kChunks / 64;
+  const int lp = lp0 + blockIdx.x;
+  const int layer = blockIdx.y / n_kv_heads, head = blockIdx.y % n_kv_heads;
+  const int page = d_pages[blockIdx.x];
+  const uint16_t* src = wire + ((static_cast<size_t>(layer) * n_lpages + lp) * n_kv_heads + head) *
+                                   static_cast<size_t>(2 * kPageTokens * D);
+  uint16_t* dst = pool + block_elem<D>(layer, page, head, n_pages, n_kv_heads);
+  const int64_t rem = len - static_cast<int64_t>(lp) * kPageTokens;
+  const int valid = rem < kPageTokens ? static_cast<int>(rem) : kPageTokens;
+  uint4 x[kPerLane];
+#pragma unroll
+  for (int j = 0; j < kPerLane; ++j) x[j] = ld16(src + 8 * (threadIdx.x + 64 * j));
+#pragma unroll
+  for (int j = 0; j < kPerLane; ++j) {
+    const int i = threadIdx.x + 64 * j;
+    st16(dst + 8 * i, valid < kPageTokens ? mask_tail<D>(x[j], i, valid) : x[j]);
+  }
+  if (blockIdx.y == 0 && threadIdx.x == 0) pt_row[lp] = page;
+}
+
+// ---------------------------------------------------------------------------------------------
+template <typename F>
+static hipError_t by_dim(int D, F&& f) {
+  if (D == 64) return f(std::integral_constant<int, 64>{});
+  if (D == 128) return f(std::integral_constant<int, 128>{});
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_append(const PoolGeom& g, const PageChunk* d_chunks, int n_chunks, const void* k,
+                         const void* v, int64_t src_rows, hipStream_t stream) {
+  if (n_chunks == 0) return hipSuccess;
+  return by_dim(g.head_dim, [&](auto dc) {
+    constexpr int D = decltype(dc)::value;
+    dim3 grid(n_chunks, g.n_layers * g.n_kv_heads);
+    kv_append_kernel<D><<<grid, 64, 0, stream>>>(
+        d_chunks, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), src_rows,
+        static_cast<uint16_t*>(g.pool), g.n_pages, g.n_kv_heads, g.page_table, g.max_pages);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_pack(const PoolGeom& g, int slot, int64_t len, void* wire, hipStream_t stream) {
+  const int n_lpages = static_cast<int>(pages_for(len));
+  if (n_lpages == 0) return hipSuccess;
+  return by_dim(g.head_dim, [&](auto dc) {
+    constexpr int D = decltype(dc)::value;
+    dim3 grid(n_lpages, g.n_layers * g.n_kv_heads);
+    kv_pack_kernel<D><<<grid, 64, 0, stream>>>(
+        static_cast<const uint16_t*>(g.pool), g.n_pages, g.n_kv_heads,
+        g.page_table + static_cast<size_t>(slot) * g.max_pages, len, static_cast<uint16_t*>(wire),
+        n_lpages);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_unpack(const PoolGeom& g, const void* wire, const int32_t* d_pages, int slot,
+                         int64_t len, int lp0, int n_lp, hipStream_t stream) {
+  const int n_lpages = static_cast<int>(pages_for(len));
+  if (n_lp == 0) return hipSuccess;
+  return by_dim(g.head_dim, [&](auto dc) {
+    constexpr int D = decltype(dc)::value;
+    dim3 grid(n_lp, g.n_layers * g.n_kv_heads);
+    kv_unpack_kernel<D><<<grid, 64, 0, stream>>>(
+        static_cast<const uint16_t*>(wire), d_pages, len, static_cast<uint16_t*>(g.pool),
+        g.n_pages, g.n_kv_heads, g.page_table + static_cast<size_t>(slot) * g.max_pages, n_lpages,
+        lp0);
+    return hipGetLastError();
+  });
+}
+
+}  // namespace cs

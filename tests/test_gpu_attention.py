@@ -1,0 +1,188 @@
+"""GPU parity of turn-1 prefill, extend and batched decode against the fp64 oracle.
+
+Sizes span several 64-query / 64-key tiles, page boundaries, ragged tails and the degenerate cases
+(L = 1, q_len = 1, q_len = L, empty batch). Tolerance per call: max-abs 1e-2, rel-L2 3e-3.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle.attention import attend_last
+from tests.helpers import assert_close, f64, kv_tokens, q_tokens, errors
+
+pytestmark = pytest.mark.gpu
+
+SEED = 777
+
+
+def _pool(hq, hkv, d, n_pages, seed=3, max_convs=64, max_pages=4096, n_layers=1):
+    from paper_2606_01839_amd import KVPool
+    return KVPool(n_layers, hq, hkv, d, n_pages=n_pages, max_convs=max_convs,
+                  max_pages_per_conv=max_pages, placement_seed=seed, device="cuda")
+
+
+def _fill(pool, conv, cid, L, hkv, d, scales=(None, None)):
+    k, v = kv_tokens(SEED, cid, 1, 0, L, hkv, d, k_scale=scales[0], v_scale=scales[1])
+    if L:
+        pool.kv_append(conv, k.cuda(), v.cuda())
+    return k, v
+
+
+def _extend_case(hq, hkv, d, prefixes, chunks, pool_seed=3, scales=(None, None)):
+    pages = sum((p + c + 15) // 16 for p, c in zip(prefixes, chunks)) + 8
+    pool = _pool(hq, hkv, d, pages, seed=pool_seed)
+    convs, kvs, qs = [], [], []
+    for i, (P, n) in enumerate(zip(prefixes, chunks)):
+        c = pool.conv_create()
+        k, v = _fill(pool, c, i, P + n, hkv, d, scales)
+        convs.append(c)
+        kvs.append((k, v))
+        qs.append(q_tokens(SEED, i, 0, P, n, hq, d))
+    q = torch.cat(qs).cuda()
+    if all(P == 0 for P in prefixes):
+        out = pool.attn_prefill_turn1(convs, chunks, 0, q)
+    else:
+        out = pool.attn_extend(convs, chunks, 0, q)
+    torch.cuda.synchronize()
+    row = 0
+    for i, n in enumerate(chunks):
+        ref = attend_last(f64(qs[i]), f64(kvs[i][0][0]), f64(kvs[i][1][0]))
+        assert_close(out[row:row + n], ref, f"conv {i} prefix {prefixes[i]} chunk {n}")
+        row += n
+    pool.close()
+    return out
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (4, 2, 64), (16, 8, 128), (8, 1, 64), (4, 4, 64)])
+def test_prefill_turn1_ragged(hq, hkv, d):
+    _extend_case(hq, hkv, d, [0, 0, 0, 0, 0], [1, 17, 64, 130, 333])
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (4, 2, 64)])
+def test_extend_against_prefix(hq, hkv, d):
+    _extend_case(hq, hkv, d, [1, 15, 64, 100, 1000, 2047], [1, 64, 65, 127, 200, 77])
+
+
+def test_extend_with_head_scales():
+    sk = np.array([0.5, 0.9, 1.3, 2.0, 1.0, 0.7, 1.7, 1.1], dtype=np.float32)
+    sv_ = np.array([2.0, 0.6, 1.0, 1.5, 0.5, 1.9, 0.8, 1.2], dtype=np.float32)
+    _extend_case(32, 8, 128, [300, 900], [256, 96], scales=(sk, sv_))
+
+
+def _decode_case(hq, hkv, d, lens, pool_seed=3, scales=(None, None)):
+    pages = sum((L + 15) // 16 for L in lens) + 8
+    pool = _pool(hq, hkv, d, pages, seed=pool_seed)
+    convs, kvs = [], []
+    for i, L in enumerate(lens):
+        c = pool.conv_create()
+        kvs.append(_fill(pool, c, i, L, hkv, d, scales))
+        convs.append(c)
+    q = torch.cat([q_tokens(SEED, i, 0, L - 1, 1, hq, d) for i, L in enumerate(lens)]).cuda()
+    out = pool.attn_decode_batch(convs, 0, q)
+    torch.cuda.synchronize()
+    for i, L in enumerate(lens):
+        ref = attend_last(f64(q[i:i + 1].cpu()), f64(kvs[i][0][0]), f64(kvs[i][1][0]))
+        assert_close(out[i:i + 1], ref, f"decode conv {i} L {L}")
+    res = out.clone()
+    pool.close()
+    return res, q
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (4, 2, 64), (8, 8, 64), (16, 8, 128)])
+def test_decode_ragged(hq, hkv, d):
+    _decode_case(hq, hkv, d, [1, 2, 15, 16, 17, 31, 32, 33, 100, 511, 512, 513, 1024, 1025, 3000])
+
+
+def test_decode_long_contexts_few_convs():
+    sk = np.linspace(0.5, 2.0, 8).astype(np.float32)
+    _decode_case(32, 8, 128, [9000, 20000], scales=(sk, sk[::-1].copy()))
+
+
+def test_decode_bitwise_deterministic_and_placement_invariant():
+    lens = [5, 700, 1500, 2600]
+    a, _ = _decode_case(32, 8, 128, lens, pool_seed=1)
+    b, _ = _decode_case(32, 8, 128, lens, pool_seed=1)
+    c, _ = _decode_case(32, 8, 128, lens, pool_seed=12345)
+    assert torch.equal(a, b), "decode is not bitwise deterministic"
+    assert torch.equal(a, c), "decode depends on physical page placement"
+
+
+def test_extend_bitwise_placement_invariant():
+    a = _extend_case(32, 8, 128, [0, 500], [200, 150], pool_seed=1)
+    b = _extend_case(32, 8, 128, [0, 500], [200, 150], pool_seed=777)
+    assert torch.equal(a, b)
+
+
+def test_decode_matches_extend_of_one_and_last_prefill_row():
+    hq, hkv, d = 32, 8, 128
+    L = 777
+    pool = _pool(hq, hkv, d, 80)
+    c = pool.conv_create()
+    _fill(pool, c, 0, L, hkv, d)
+    qall = q_tokens(SEED, 0, 0, 0, L, hq, d).cuda()
+    full = pool.attn_prefill_turn1([c], [L], 0, qall)
+    ext = pool.attn_extend([c], [1], 0, qall[-1:].contiguous())
+    dec = pool.attn_decode_batch([c], 0, qall[-1:].contiguous())
+    torch.cuda.synchronize()
+    for x, y in [(full[-1:], ext), (ext, dec), (full[-1:], dec)]:
+        m, r = errors(x, f64(y))
+        assert m <= 1e-2 and r <= 3e-3
+    pool.close()
+
+
+def test_chunked_extend_matches_one_shot_prefill():
+    hq, hkv, d = 32, 8, 128
+    L = 640
+    cuts = [0, 100, 101, 333, 640]
+    pool = _pool(hq, hkv, d, 100)
+    one = pool.conv_create()
+    k, v = kv_tokens(SEED, 0, 1, 0, L, hkv, d)
+    pool.kv_append(one, k.cuda(), v.cuda())
+    q = q_tokens(SEED, 0, 0, 0, L, hq, d).cuda()
+    full = pool.attn_prefill_turn1([one], [L], 0, q)
+    ch = pool.conv_create()
+    parts = []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        pool.kv_append(ch, k[:, a:b].contiguous().cuda(), v[:, a:b].contiguous().cuda())
+        parts.append(pool.attn_extend([ch], [b - a], 0, q[a:b].contiguous()))
+    torch.cuda.synchronize()
+    m, r = errors(torch.cat(parts), f64(full))
+    assert m <= 1e-2 and r <= 3e-3
+    pool.close()
+
+
+def test_nan_poisoned_pool_does_not_leak():
+    """Every page starts as NaN; appends zero their pages' tails, so nothing past a conversation's
+    end (or in never-used pages) can reach the outputs."""
+    hq, hkv, d = 32, 8, 128
+    lens = [1, 17, 300]
+    pool = _pool(hq, hkv, d, 40)
+    pool.kv.view(torch.int16).fill_(0x7FC0)  # bf16 quiet NaN everywhere
+    convs, kvs = [], []
+    for i, L in enumerate(lens):
+        c = pool.conv_create()
+        kvs.append(_fill(pool, c, i, L, hkv, d))
+        convs.append(c)
+    q = torch.cat([q_tokens(SEED, i, 0, L - 1, 1, hq, d) for i, L in enumerate(lens)]).cuda()
+    out = pool.attn_decode_batch(convs, 0, q)
+    qp = torch.cat([q_tokens(SEED, i, 0, 0, L, hq, d) for i, L in enumerate(lens)]).cuda()
+    outp = pool.attn_prefill_turn1(convs, lens, 0, qp)
+    torch.cuda.synchronize()
+    row = 0
+    for i, L in enumerate(lens):
+        ref = attend_last(f64(q[i:i + 1].cpu()), f64(kvs[i][0][0]), f64(kvs[i][1][0]))
+        assert_close(out[i:i + 1], ref, f"poisoned decode {i}")
+        refp = attend_last(f64(qp[row:row + L].cpu()), f64(kvs[i][0][0]), f64(kvs[i][1][0]))
+        assert_close(outp[row:row + L], refp, f"poisoned prefill {i}")
+        row += L
+    pool.close()
+
+
+def test_empty_batches_are_noops():
+    pool = _pool(32, 8, 128, 8)
+    c = pool.conv_create()
+    _fill(pool, c, 0, 20, 8, 128)
+    q0 = torch.empty(0, 32, 128, dtype=torch.bfloat16, device="cuda")
+    assert pool.attn_decode_batch([], 0, q0).shape == (0, 32, 128)
+    assert pool.attn_extend([c], [0], 0, q0).shape == (0, 32, 128)
+    pool.close()
