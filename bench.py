@@ -1,0 +1,398 @@
+#!/usr/bin/env python3
+"""Benchmark of the paged-KV attention hot path on one MI355X.
+
+Headline workload (the one `value` is quoted on): batched single-token decode over 64
+conversations with cached contexts uniform in [8192, 32768] tokens, 32 query / 8 KV heads,
+head_dim 128, bf16 K/V with per-KV-head scales in [0.5, 2], 16-token pages placed at random,
+one layer. One step = one `attn_decode_batch` call (split-K kernel + merge kernel) with all
+inputs already resident in HBM. `value` = algorithmic bytes of a step (K and V read once,
+Q, O, page-table entries) / measured step time.
+
+Extra components (same JSON line, "components"): extend-prefill of 16 conversations
+(prefix U[16384, 65536], chunk log-normal median 1024 in [128, 4096]), turn-1 prefill of 8
+conversations (L U[32768, 131072]) and its one-time KV transfer (pack + unpack), and KV append.
+
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--skip-components]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from synth import values as sv  # noqa: E402
+from synth.traces import (DecodeBatch, ExtendBatch, PrefillTransfer, KIND_K, KIND_Q,  # noqa: E402
+                          KIND_V, pages_for)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
+METRIC = "decode-attn HBM GB/s + extend/prefill TFLOP/s, each as % of MI355X peak"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_split_traffic.json")
+KERNEL_SOURCES = ["paper_2606_01839_amd/csrc/decode.hip", "paper_2606_01839_amd/csrc/device_common.hpp"]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def gen_kv(seed, conv, start, n, hkv, d, sk=None, sv_=None, device="cuda"):
+    per = hkv * d
+    k = sv.bf16_tensor(sv.mix_key(seed, conv, KIND_K, 0), (n, hkv, d), head_scale=sk,
+                       start=start * per, device=device)
+    v = sv.bf16_tensor(sv.mix_key(seed, conv, KIND_V, 0), (n, hkv, d), head_scale=sv_,
+                       start=start * per, device=device)
+    return k, v
+
+
+def gen_q(seed, conv, start, n, hq, d, device="cuda"):
+    return sv.bf16_tensor(sv.mix_key(seed, conv, KIND_Q, 0), (n, hq, d), start=start * hq * d,
+                          device=device)
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_per_launch(workload: str):
+    """HBM bytes per decode-split launch from committed rocprofv3 counters, if the kernel source
+    is unchanged since they were taken (else None)."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != source_hash() or t.get("workload") != workload:
+        return None
+    return t.get("traffic_bytes_per_launch")
+
+
+def timed(fn, steps, warmup):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps * 1e3
+
+
+def profiled(pool, fn, steps):
+    pool.profile_start()
+    for _ in range(steps):
+        fn()
+    return pool.profile_stop()
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas"]
+        if n:
+            return int(max(n))
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0))
+
+
+# ------------------------------------------------------------------------------------------------
+# headline: decode batch
+# ------------------------------------------------------------------------------------------------
+def bench_decode(args):
+    from paper_2606_01839_amd import KVPool
+    tr = DecodeBatch()
+    sh = tr.shape
+    hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    lens = tr.lengths().astype(np.int64)
+    sk, svs = tr.head_scales()
+    n_pages = int(sum(pages_for(L) for L in lens) * 1.1)
+    pool = KVPool(1, hq, hkv, d, n_pages=n_pages, max_convs=tr.batch,
+                  max_pages_per_conv=pages_for(tr.hi), placement_seed=tr.seed + 1)
+    convs, kv_dev = [], []
+    t0 = time.perf_counter()
+    for b, L in enumerate(lens):
+        c = pool.conv_create()
+        k, v = gen_kv(tr.seed, b, 0, int(L), hkv, d, sk, svs)
+        pool.kv_append(c, k[None], v[None])
+        convs.append(c)
+        kv_dev.append((k, v))
+    q = torch.cat([gen_q(tr.seed, b, int(L) - 1, 1, hq, d) for b, L in enumerate(lens)])
+    out = torch.empty_like(q)
+    torch.cuda.synchronize()
+    log(f"decode: filled {len(lens)} conversations ({lens.sum()} tokens) in {time.perf_counter() - t0:.1f}s")
+
+    step = lambda: pool.attn_decode_batch(convs, 0, q, out)
+    ms = timed(step, args.steps, args.warmup)
+    prof = profiled(pool, step, args.steps)
+    split_ms = prof["decode_split"][0] / max(1, prof["decode_split"][1])
+    merge_ms = prof["decode_merge"][0] / max(1, prof["decode_merge"][1])
+
+    kv_bytes = int(lens.sum()) * 2 * hkv * d * 2
+    q_bytes = len(lens) * hq * d * 2
+    pt_bytes = int(sum(pages_for(L) for L in lens)) * 4
+    step_bytes = kv_bytes + 2 * q_bytes + pt_bytes
+    split_bytes = kv_bytes + q_bytes + pt_bytes
+    out_host = out.cpu()
+
+    # parity of every conversation against the oracle, and the oracle's own time (CPU baseline)
+    from oracle.attention import attend_rows
+    max_abs, num, den = 0.0, 0.0, 0.0
+    cpu_s = 0.0
+    # the device-generated inputs are the seeded generator's values: check two against the host
+    for b in (int(np.argmin(lens)), int(np.argmax(lens))):
+        L = int(lens[b])
+        kh, vh = gen_kv(tr.seed, b, 0, min(L, 4096), hkv, d, sk, svs, device="cpu")
+        assert torch.equal(kh, kv_dev[b][0][:min(L, 4096)].cpu()) and torch.equal(vh, kv_dev[b][1][:min(L, 4096)].cpu())
+    for b, L in enumerate(lens):
+        kf = sv.bf16_to_f64(kv_dev[b][0])
+        vf = sv.bf16_to_f64(kv_dev[b][1])
+        qf = sv.bf16_to_f64(q[b:b + 1])
+        t = time.perf_counter()
+        ref = attend_rows(qf, [int(L) - 1], kf, vf)
+        cpu_s += time.perf_counter() - t
+        diff = sv.bf16_to_f64(out_host[b:b + 1]) - ref
+        max_abs = max(max_abs, float(np.abs(diff).max()))
+        num += float((diff ** 2).sum())
+        den += float((ref ** 2).sum())
+    rel_l2 = math.sqrt(num / den)
+    workload = (f"decode batch: {len(lens)} conversations, context U[{tr.lo},{tr.hi}] (sum "
+                f"{int(lens.sum())} tokens), {hq}q/{hkv}kv heads, head_dim {d}, bf16 K/V x per-head "
+                f"scale U[{tr.scale_lo},{tr.scale_hi}], 16-token pages randomly placed, 1 layer")
+    traffic = traffic_per_launch(workload)
+    res = {
+        "ms_per_step": ms,
+        "value_gbs": step_bytes / (ms * 1e-3) / 1e9,
+        "split_ms": split_ms,
+        "merge_ms": merge_ms,
+        "split_bytes": split_bytes,
+        "step_bytes": step_bytes,
+        "workload": workload,
+        "traffic": traffic,
+        "parity": {"convs": len(lens), "max_abs": max_abs, "rel_l2": rel_l2,
+                   "ok": bool(max_abs <= 1e-2 and rel_l2 <= 3e-3)},
+        "cpu": {"value": step_bytes / cpu_s / 1e9, "unit": "GB/s", "cores": blas_threads(),
+                "kind": "oracle",
+                "sample": f"fp64 oracle over all {len(lens)} conversations x {hq} heads of the same "
+                          f"decode step (inputs already in host memory as fp64); {cpu_s:.2f} s"},
+    }
+    pool.close()
+    del kv_dev
+    torch.cuda.empty_cache()
+    return res
+
+
+# ------------------------------------------------------------------------------------------------
+# components: extend-prefill, turn-1 prefill + transfer, append
+# ------------------------------------------------------------------------------------------------
+def attn_flops(prefix, n, hq, d):
+    pairs = sum(int(nn) * int(P) + int(nn) * (int(nn) + 1) // 2 for P, nn in zip(prefix, n))
+    return 4 * d * hq * pairs
+
+
+def bench_extend(args):
+    from paper_2606_01839_amd import KVPool
+    tr = ExtendBatch()
+    sh = tr.shape
+    hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    prefix, chunk = tr.lengths()
+    total = prefix + chunk
+    pool = KVPool(1, hq, hkv, d, n_pages=int(sum(pages_for(L) for L in total)) + 64,
+                  max_convs=tr.n_convs, max_pages_per_conv=pages_for(int(total.max())),
+                  placement_seed=tr.seed + 1)
+    convs = []
+    for b in range(tr.n_convs):
+        c = pool.conv_create()
+        k, v = gen_kv(tr.seed, b, 0, int(prefix[b]), hkv, d)
+        pool.kv_append(c, k[None], v[None])
+        convs.append(c)
+        del k, v
+    # the turn's new tokens are appended (timed separately), then attend
+    new_kv = [gen_kv(tr.seed, b, int(prefix[b]), int(chunk[b]), hkv, d) for b in range(tr.n_convs)]
+    kcat = torch.cat([k for k, _ in new_kv])[None].contiguous()
+    vcat = torch.cat([v for _, v in new_kv])[None].contiguous()
+    torch.cuda.synchronize()
+    pool.profile_start()
+    pool.kv_append_batch(convs, chunk, kcat, vcat)
+    app = pool.profile_stop()["append"]
+    q = torch.cat([gen_q(tr.seed, b, int(prefix[b]), int(chunk[b]), hq, d) for b in range(tr.n_convs)])
+    out = torch.empty_like(q)
+    step = lambda: pool.attn_extend(convs, chunk, 0, q, out)
+    reps = max(3, args.steps // 4)
+    ms = timed(step, reps, 1)
+    prof = profiled(pool, step, reps)
+    fwd_ms = prof["attn_fwd"][0] / max(1, prof["attn_fwd"][1])
+    flops = attn_flops(prefix, chunk, hq, d)
+    app_bytes = 2 * int(chunk.sum()) * 2 * hkv * d * 2    # read + write of the new K and V
+    # light parity: the last query row of the first and last conversations
+    from oracle.attention import attend_rows
+    ok = True
+    for b in (0, tr.n_convs - 1):
+        L = int(total[b])
+        kf, vf = (sv.bf16_to_f64(t) for t in gen_kv(tr.seed, b, 0, L, hkv, d, device="cpu"))
+        row = int(chunk[:b + 1].sum()) - 1
+        ref = attend_rows(sv.bf16_to_f64(q[row:row + 1]), [L - 1], kf, vf)
+        err = np.abs(sv.bf16_to_f64(out[row:row + 1]) - ref).max()
+        ok = ok and err <= 1e-2
+    pool.close()
+    del new_kv, kcat, vcat
+    torch.cuda.empty_cache()
+    return {
+        "extend": {"workload": f"extend-prefill: {tr.n_convs} conversations, prefix U[{tr.prefix_lo},"
+                               f"{tr.prefix_hi}], chunk logN(median {tr.chunk_median}) in "
+                               f"[{tr.chunk_lo},{tr.chunk_hi}] (sum {int(chunk.sum())}), {hq}q/{hkv}kv, d {d}",
+                   "ms": ms, "kernel_ms": fwd_ms, "flops": flops,
+                   "tflops": flops / (ms * 1e-3) / 1e12,
+                   "roofline": {"bound": "mfma", "achieved": flops / (fwd_ms * 1e-3) / 1e12,
+                                "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
+                   "spot_parity_ok": bool(ok)},
+        "append": {"workload": f"kv_append of the {int(chunk.sum())} new tokens of the extend batch",
+                   "kernel_ms": app[0], "bytes": app_bytes,
+                   "gbs": app_bytes / (app[0] * 1e-3) / 1e9,
+                   "roofline": {"bound": "hbm", "achieved": app_bytes / (app[0] * 1e-3) / 1e9,
+                                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                "frac": app_bytes / (app[0] * 1e-3) / 1e9 / HBM_PEAK_GBS}},
+    }
+
+
+def bench_prefill_transfer(args):
+    from paper_2606_01839_amd import KVPool
+    tr = PrefillTransfer()
+    sh = tr.shape
+    hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    lens = tr.lengths().astype(np.int64)
+    npg = int(sum(pages_for(L) for L in lens)) + 64
+    mk = lambda seed: KVPool(1, hq, hkv, d, n_pages=npg, max_convs=tr.n_convs,
+                             max_pages_per_conv=pages_for(tr.hi), placement_seed=seed)
+    pre = mk(tr.seed + 1)
+    convs = []
+    for b, L in enumerate(lens):
+        c = pre.conv_create()
+        k, v = gen_kv(tr.seed, b, 0, int(L), hkv, d)
+        pre.kv_append(c, k[None], v[None])
+        convs.append(c)
+        del k, v
+    q = torch.cat([gen_q(tr.seed, b, 0, int(L), hq, d) for b, L in enumerate(lens)])
+    out = torch.empty_like(q)
+    step = lambda: pre.attn_prefill_turn1(convs, lens, 0, q, out)
+    reps = 2
+    ms = timed(step, reps, 1)
+    prof = profiled(pre, step, reps)
+    fwd_ms = prof["attn_fwd"][0] / max(1, prof["attn_fwd"][1])
+    flops = attn_flops([0] * len(lens), lens, hq, d)
+    # one-time transfer: pack every conversation, unpack into a pool with other placement
+    dst = mk(tr.dst_seed)
+    wires = [torch.empty(pre.kv_pack_size(c), dtype=torch.uint8, device="cuda") for c in convs]
+    pre.profile_start()
+    for c, w in zip(convs, wires):
+        pre.kv_pack(c, w)
+    pk = pre.profile_stop()["pack"]
+    dst.profile_start()
+    dconvs = [dst.kv_unpack(w, int(L)) for w, L in zip(wires, lens)]
+    up = dst.profile_stop()["unpack"]
+    ok = True
+    for c, w in zip(dconvs, wires):
+        ok = ok and torch.equal(dst.kv_pack(c), w)
+    torch.cuda.synchronize()
+    move = 2 * int(lens.sum()) * 2 * hkv * d * 2          # read + write of every valid token's K, V
+    pre.close()
+    dst.close()
+    del wires, q, out
+    torch.cuda.empty_cache()
+    gbs = lambda b, t: b / (t * 1e-3) / 1e9
+    return {
+        "prefill": {"workload": f"turn-1 prefill: {tr.n_convs} conversations, L U[{tr.lo},{tr.hi}] "
+                                f"(sum {int(lens.sum())}), {hq}q/{hkv}kv, d {d}",
+                    "ms": ms, "kernel_ms": fwd_ms, "flops": flops,
+                    "tflops": flops / (ms * 1e-3) / 1e12,
+                    "roofline": {"bound": "mfma", "achieved": flops / (fwd_ms * 1e-3) / 1e12,
+                                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                 "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS}},
+        "pack": {"kernel_ms": pk[0], "launches": pk[1], "bytes": move, "gbs": gbs(move, pk[0]),
+                 "roofline": {"bound": "hbm", "achieved": gbs(move, pk[0]), "peak": HBM_PEAK_GBS,
+                              "unit": "GB/s", "frac": gbs(move, pk[0]) / HBM_PEAK_GBS}},
+        "unpack": {"kernel_ms": up[0], "launches": up[1], "bytes": move, "gbs": gbs(move, up[0]),
+                   "roofline": {"bound": "hbm", "achieved": gbs(move, up[0]), "peak": HBM_PEAK_GBS,
+                                "unit": "GB/s", "frac": gbs(move, up[0]) / HBM_PEAK_GBS},
+                   "round_trip_bit_exact": bool(ok)},
+    }
+
+
+def copy_calibration():
+    """A plain 1 GiB device copy: its FETCH_SIZE / WRITE_SIZE counters calibrate the HBM traffic
+    reported for the decode kernel (known 1 GiB read + 1 GiB written)."""
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--skip-components", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB copy (for counter calibration under rocprofv3)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the hot path shards by conversation with no exchange "
+              "on the hot path, and this build runs on a single MI355X (use --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    from paper_2606_01839_amd import load_library
+    load_library()
+    if args.calibrate_copy:
+        copy_calibration()
+    dec = bench_decode(args)
+    comps = {}
+    if not args.skip_components:
+        comps.update(bench_extend(args))
+        comps.update(bench_prefill_transfer(args))
+    split_gbs = dec["split_bytes"] / (dec["split_ms"] * 1e-3) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": round(dec["value_gbs"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dec["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded counter-based generator; no dataset)",
+        "config": {"workload": dec["workload"], "global_batch": 64, "seq_len": "8192-32768",
+                   "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "kernel": "decode_split_kernel<128>",
+                     "achieved": round(split_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(split_gbs / HBM_PEAK_GBS, 4), "traffic": dec["traffic"],
+                     "algorithmic_bytes_per_launch": dec["split_bytes"],
+                     "kernel_ms": round(dec["split_ms"], 4), "merge_kernel_ms": round(dec["merge_ms"], 4)},
+        "cpu_baseline": dec["cpu"],
+        "parity": dec["parity"],
+        "components": comps,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -186,6 +186,25 @@ cs_status cs_kv_pack(const cs_pool* pool, cs_conv conv, void* dst, size_t dst_by
 cs_status cs_kv_unpack(cs_pool* pool, const void* src, size_t src_bytes, int64_t n_tokens,
                        cs_conv* out_conv, cs_stream stream);
 
+/*
+ * Instrumentation (per-kernel timing; not part of the attention path). Between cs_profile_start
+ * and cs_profile_stop every kernel the pool launches is bracketed by two HIP timing events on its
+ * stream. cs_profile_stop waits for those events, writes the summed milliseconds and the launch
+ * count per kernel kind into ms[CS_PROF_KINDS] and launches[CS_PROF_KINDS], and disables timing.
+ * Errors: CS_EINVAL (null), CS_EHIP.
+ */
+enum {
+  CS_PROF_APPEND = 0,        /* kv append kernel */
+  CS_PROF_PACK = 1,          /* kv pack kernel */
+  CS_PROF_UNPACK = 2,        /* kv unpack kernel */
+  CS_PROF_DECODE_SPLIT = 3,  /* decode split-K kernel */
+  CS_PROF_DECODE_MERGE = 4,  /* decode merge kernel */
+  CS_PROF_ATTN_FWD = 5,      /* prefill / extend attention kernel */
+  CS_PROF_KINDS = 6
+};
+cs_status cs_profile_start(cs_pool* pool);
+cs_status cs_profile_stop(cs_pool* pool, double* ms, int64_t* launches);
+
 /* Message of the last failing call on this thread ("" if none). Valid until the next call. */
 const char* cs_last_error(void);
 

@@ -24,8 +24,10 @@ EXPORTS = [
     "cs_pool_kv_bytes", "cs_pool_workspace_bytes", "cs_pool_create", "cs_pool_destroy",
     "cs_pool_occupancy", "cs_conv_create", "cs_conv_destroy", "cs_conv_len", "cs_conv_pages",
     "cs_kv_append", "cs_kv_append_batch", "cs_attn_prefill_turn1", "cs_attn_extend",
-    "cs_attn_decode_batch", "cs_kv_pack_size", "cs_kv_pack", "cs_kv_unpack", "cs_last_error",
+    "cs_attn_decode_batch", "cs_kv_pack_size", "cs_kv_pack", "cs_kv_unpack", "cs_profile_start",
+    "cs_profile_stop", "cs_last_error",
 ]
+PROFILE_KINDS = ["append", "pack", "unpack", "decode_split", "decode_merge", "attn_fwd"]
 
 
 class ConserveError(RuntimeError):
@@ -74,6 +76,8 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "cs_kv_pack_size": (I32, [P, I32, ctypes.POINTER(SZ)]),
         "cs_kv_pack": (I32, [P, I32, VP, SZ, VP]),
         "cs_kv_unpack": (I32, [P, VP, SZ, I64, PI32, VP]),
+        "cs_profile_start": (I32, [P]),
+        "cs_profile_stop": (I32, [P, ctypes.POINTER(ctypes.c_double), PI64]),
         "cs_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sigs.items():
@@ -254,6 +258,18 @@ class KVPool:
         _check(self.lib.cs_attn_decode_batch(self._handle, ca.size, cp, layer, qptr, optr,
                                              _stream_handle(self.device)))
         return out
+
+    # -- instrumentation -----------------------------------------------------------------------
+    def profile_start(self) -> None:
+        _check(self.lib.cs_profile_start(self._handle))
+
+    def profile_stop(self) -> dict:
+        """{kernel kind: (total ms, launches)} for kernels launched since profile_start."""
+        n = len(PROFILE_KINDS)
+        ms = (ctypes.c_double * n)()
+        cnt = (ctypes.c_int64 * n)()
+        _check(self.lib.cs_profile_stop(self._handle, ms, cnt))
+        return {k: (ms[i], cnt[i]) for i, k in enumerate(PROFILE_KINDS)}
 
     # -- one-time transfer ---------------------------------------------------------------------
     def kv_pack_size(self, conv: int) -> int:

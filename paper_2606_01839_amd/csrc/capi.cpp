@@ -95,6 +95,14 @@ struct cs_pool {
   hipEvent_t switch_ev = nullptr;
   hipStream_t stream = nullptr;
   bool have_stream = false;
+  // instrumentation: timing events around each kernel launch while enabled
+  struct ProfEvent {
+    hipEvent_t start, stop;
+    int kind;
+  };
+  bool prof_on = false;
+  std::vector<hipEvent_t> ev_free;
+  std::vector<ProfEvent> prof_events;
 
   cs_pool(const cs_pool_desc& d, char* kvp, size_t kvb, char* wsp, size_t wsb, uint64_t seed)
       : desc(d), kv(kvp), kv_bytes(kvb), ws(wsp), ws_bytes(wsb), lay(ws_layout(d)),
@@ -161,6 +169,32 @@ cs_status use_stream(cs_pool* p, hipStream_t s) {
   }
   p->stream = s;
   p->have_stream = true;
+  return CS_OK;
+}
+
+hipError_t take_event(cs_pool* p, hipEvent_t* e) {
+  if (!p->ev_free.empty()) {
+    *e = p->ev_free.back();
+    p->ev_free.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(e);
+}
+
+// Launch a kernel; while profiling, bracket it with timing events on the pool's stream.
+template <typename F>
+cs_status timed_launch(cs_pool* p, int kind, const char* what, F&& launch) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (p->prof_on) {
+    CS_HIP(take_event(p, &a), "hipEventCreate");
+    CS_HIP(take_event(p, &b), "hipEventCreate");
+    CS_HIP(hipEventRecord(a, p->stream), "hipEventRecord");
+  }
+  CS_HIP(launch(), what);
+  if (p->prof_on) {
+    CS_HIP(hipEventRecord(b, p->stream), "hipEventRecord");
+    p->prof_events.push_back({a, b, kind});
+  }
   return CS_OK;
 }
 
@@ -281,8 +315,10 @@ cs_status attend(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* q_l
     cs::ExtendConvDesc* dc = nullptr;
     cs::ExtendTile* dt = nullptr;
     if ((st = upload2(p, plan.convs, part, &dc, &dt)) != CS_OK) return st;
-    CS_HIP(cs::launch_extend(g, layer, dc, dt, static_cast<int>(part.size()), q, out, p->stream),
-           "attention launch");
+    st = timed_launch(p, CS_PROF_ATTN_FWD, "attention launch", [&] {
+      return cs::launch_extend(g, layer, dc, dt, static_cast<int>(part.size()), q, out, p->stream);
+    });
+    if (st != CS_OK) return st;
   }
   return CS_OK;
 }
@@ -332,9 +368,11 @@ cs_status append_impl(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t
     const size_t c1 = std::min(chunks.size(), c0 + per);
     void* d = nullptr;
     if ((st = upload(p, chunks.data() + c0, (c1 - c0) * sizeof(cs::PageChunk), &d)) != CS_OK) return st;
-    CS_HIP(cs::launch_append(g, static_cast<const cs::PageChunk*>(d), static_cast<int>(c1 - c0), k, v,
-                             total, p->stream),
-           "append launch");
+    st = timed_launch(p, CS_PROF_APPEND, "append launch", [&] {
+      return cs::launch_append(g, static_cast<const cs::PageChunk*>(d), static_cast<int>(c1 - c0), k, v,
+                               total, p->stream);
+    });
+    if (st != CS_OK) return st;
   }
   return CS_OK;
 }
@@ -380,6 +418,11 @@ cs_status cs_pool_destroy(cs_pool* p) {
     if (p->have_stream && hipStreamSynchronize(p->stream) != hipSuccess)
       st = fail(CS_EHIP, "hipStreamSynchronize failed while destroying the pool");
     for (auto& e : p->quarter_ev) (void)hipEventDestroy(e);
+    for (auto& e : p->ev_free) (void)hipEventDestroy(e);
+    for (auto& pe : p->prof_events) {
+      (void)hipEventDestroy(pe.start);
+      (void)hipEventDestroy(pe.stop);
+    }
     (void)hipEventDestroy(p->switch_ev);
     (void)hipHostFree(p->h_ring);
   }
@@ -471,10 +514,16 @@ cs_status cs_attn_decode_batch(cs_pool* p, int32_t n, const cs_conv* convs, int3
   void* d = nullptr;
   if ((st = upload(p, plan.convs.data(), plan.convs.size() * sizeof(cs::DecodeConvDesc), &d)) != CS_OK)
     return st;
-  CS_HIP(cs::launch_decode(p->geom(), layer, static_cast<const cs::DecodeConvDesc*>(d), n, plan.n_items,
-                           plan.split_tokens, q, out, p->partials(), p->stream),
-         "decode launch");
-  return CS_OK;
+  const cs::PoolGeom g = p->geom();
+  const auto* dc = static_cast<const cs::DecodeConvDesc*>(d);
+  st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
+    return cs::launch_decode_split(g, layer, dc, n, plan.n_items, plan.split_tokens, q, p->partials(),
+                                   p->stream);
+  });
+  if (st != CS_OK) return st;
+  return timed_launch(p, CS_PROF_DECODE_MERGE, "decode merge launch", [&] {
+    return cs::launch_decode_merge(g, dc, n, p->partials(), out, p->stream);
+  });
 }
 
 cs_status cs_kv_pack_size(const cs_pool* p, cs_conv conv, size_t* bytes) {
@@ -496,8 +545,9 @@ cs_status cs_kv_pack(const cs_pool* pc, cs_conv conv, void* dst, size_t dst_byte
   cs_status st;
   if ((st = ensure_device(p)) != CS_OK) return st;
   if ((st = use_stream(p, as_stream(stream))) != CS_OK) return st;
-  CS_HIP(cs::launch_pack(p->geom(), cs::ConvTable::slot_of(conv), c->len, dst, p->stream), "pack launch");
-  return CS_OK;
+  return timed_launch(p, CS_PROF_PACK, "pack launch", [&] {
+    return cs::launch_pack(p->geom(), cs::ConvTable::slot_of(conv), c->len, dst, p->stream);
+  });
 }
 
 cs_status cs_kv_unpack(cs_pool* p, const void* src, size_t src_bytes, int64_t n_tokens,
@@ -525,10 +575,43 @@ cs_status cs_kv_unpack(cs_pool* p, const void* src, size_t src_bytes, int64_t n_
     const size_t p1 = std::min(c->pages.size(), p0 + per);
     void* d = nullptr;
     if ((st = upload(p, c->pages.data() + p0, (p1 - p0) * sizeof(int32_t), &d)) != CS_OK) return st;
-    CS_HIP(cs::launch_unpack(p->geom(), src, static_cast<const int32_t*>(d), cs::ConvTable::slot_of(h),
-                             n_tokens, static_cast<int>(p0), static_cast<int>(p1 - p0), p->stream),
-           "unpack launch");
+    st = timed_launch(p, CS_PROF_UNPACK, "unpack launch", [&] {
+      return cs::launch_unpack(p->geom(), src, static_cast<const int32_t*>(d), cs::ConvTable::slot_of(h),
+                               n_tokens, static_cast<int>(p0), static_cast<int>(p1 - p0), p->stream);
+    });
+    if (st != CS_OK) return st;
   }
+  return CS_OK;
+}
+
+cs_status cs_profile_start(cs_pool* p) {
+  if (!p) return fail(CS_EINVAL, "null pool");
+  for (auto& pe : p->prof_events) {
+    p->ev_free.push_back(pe.start);
+    p->ev_free.push_back(pe.stop);
+  }
+  p->prof_events.clear();
+  p->prof_on = true;
+  return CS_OK;
+}
+
+cs_status cs_profile_stop(cs_pool* p, double* ms, int64_t* launches) {
+  if (!p || !ms || !launches) return fail(CS_EINVAL, "null argument");
+  for (int k = 0; k < CS_PROF_KINDS; ++k) {
+    ms[k] = 0.0;
+    launches[k] = 0;
+  }
+  p->prof_on = false;
+  for (auto& pe : p->prof_events) {
+    CS_HIP(hipEventSynchronize(pe.stop), "hipEventSynchronize");
+    float t = 0.f;
+    CS_HIP(hipEventElapsedTime(&t, pe.start, pe.stop), "hipEventElapsedTime");
+    ms[pe.kind] += t;
+    launches[pe.kind] += 1;
+    p->ev_free.push_back(pe.start);
+    p->ev_free.push_back(pe.stop);
+  }
+  p->prof_events.clear();
   return CS_OK;
 }
 

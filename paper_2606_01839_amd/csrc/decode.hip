@@ -200,10 +200,9 @@ __global__ __launch_bounds__(64) void decode_merge_kernel(DecodeArgs a) {
   for (int i = 0; i < PER; ++i) orow[lane + 64 * i] = static_cast<uint16_t>(pack_bf16x2(acc[i] * inv, 0.f) & 0xFFFFu);
 }
 
-hipError_t launch_decode(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs, int n_convs,
-                         int n_items, int split_tokens, const void* q, void* out, float* partials,
-                         hipStream_t stream) {
-  if (n_convs == 0) return hipSuccess;
+static DecodeArgs make_args(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs, int n_convs,
+                            int n_items, int split_tokens, const void* q, void* out,
+                            const float* partials) {
   DecodeArgs a;
   a.pool = static_cast<const uint16_t*>(g.pool);
   a.n_pages = g.n_pages;
@@ -218,19 +217,31 @@ hipError_t launch_decode(const PoolGeom& g, int layer, const DecodeConvDesc* d_c
   a.split = split_tokens;
   a.q = static_cast<const uint16_t*>(q);
   a.out = static_cast<uint16_t*>(out);
-  a.partials = partials;
+  a.partials = const_cast<float*>(partials);
   a.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(g.head_dim)));
-  const int waves = n_items * g.n_kv_heads;
-  const int blocks = (waves + 3) / 4;
-  if (g.head_dim == 128) {
-    decode_split_kernel<128><<<blocks, 256, 0, stream>>>(a);
-    decode_merge_kernel<128><<<dim3(n_convs, g.n_q_heads), 64, 0, stream>>>(a);
-  } else if (g.head_dim == 64) {
-    decode_split_kernel<64><<<blocks, 256, 0, stream>>>(a);
-    decode_merge_kernel<64><<<dim3(n_convs, g.n_q_heads), 64, 0, stream>>>(a);
-  } else {
-    return hipErrorInvalidValue;
-  }
+  return a;
+}
+
+hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs,
+                               int n_convs, int n_items, int split_tokens, const void* q,
+                               float* partials, hipStream_t stream) {
+  if (n_convs == 0) return hipSuccess;
+  const DecodeArgs a = make_args(g, layer, d_convs, n_convs, n_items, split_tokens, q, nullptr, partials);
+  const int blocks = (n_items * g.n_kv_heads + 3) / 4;
+  if (g.head_dim == 128) decode_split_kernel<128><<<blocks, 256, 0, stream>>>(a);
+  else if (g.head_dim == 64) decode_split_kernel<64><<<blocks, 256, 0, stream>>>(a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_merge(const PoolGeom& g, const DecodeConvDesc* d_convs, int n_convs,
+                               const float* partials, void* out, hipStream_t stream) {
+  if (n_convs == 0) return hipSuccess;
+  const DecodeArgs a = make_args(g, 0, d_convs, n_convs, 0, 0, nullptr, out, partials);
+  const dim3 grid(n_convs, g.n_q_heads);
+  if (g.head_dim == 128) decode_merge_kernel<128><<<grid, 64, 0, stream>>>(a);
+  else if (g.head_dim == 64) decode_merge_kernel<64><<<grid, 64, 0, stream>>>(a);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -30,10 +30,12 @@ hipError_t launch_pack(const PoolGeom& g, int slot, int64_t len, void* wire, hip
 hipError_t launch_unpack(const PoolGeom& g, const void* wire, const int32_t* d_pages, int slot,
                          int64_t len, int lp0, int n_lp, hipStream_t stream);
 
-// Decode: split kernel over plan items, then merge.
-hipError_t launch_decode(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs, int n_convs,
-                         int n_items, int split_tokens, const void* q, void* out, float* partials,
-                         hipStream_t stream);
+// Decode: split kernel over plan items (partials), then the merge kernel (output).
+hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs,
+                               int n_convs, int n_items, int split_tokens, const void* q,
+                               float* partials, hipStream_t stream);
+hipError_t launch_decode_merge(const PoolGeom& g, const DecodeConvDesc* d_convs, int n_convs,
+                               const float* partials, void* out, hipStream_t stream);
 
 // Extend / prefill: one workgroup per (tile, kv head).
 hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,
