@@ -47,9 +47,18 @@ struct FwdSmem {
 // as one 16-byte run.
 __device__ __forceinline__ int vt_group_pos(int c) { return ((c & 1) << 1) | (c >> 1); }
 
-template <int D, int G>
-__global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
-  constexpr int NT = 64 * G;           // threads
+#ifndef CS_FWD_QT
+#define CS_FWD_QT 1  // 32-query tiles per wave: 1 -> 2G waves per workgroup, 2 -> G waves
+#endif
+
+// Lazy rescaling threshold (log2 units): the running max used in the exponent is only raised when
+// a new score exceeds it by more than this, so P <= 2^8 and the O/l rescale is rare.
+constexpr float kRescaleLog2 = 8.f;
+
+template <int D, int G, int QT>
+__global__ __launch_bounds__(64 * G * (2 / QT)) void attn_fwd_kernel(ExtendArgs a) {
+  constexpr int NW = G * (2 / QT);     // waves: G query heads x (2 / QT) query blocks
+  constexpr int NT = 64 * NW;          // threads
   constexpr int KS = D / 16;           // k-steps of QK^T (16 dims each)
   constexpr int DT = D / 32;           // 32-dim output tiles
   constexpr int CH = kBN * D / 8;      // 16-byte chunks per K (or V^T) tile
@@ -67,16 +76,20 @@ __global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
   const int n_kt = pos_max / kBN + 1;                        // key tiles 0 .. n_kt-1
   const int n_pg = (cd.len + kPageTokens - 1) / kPageTokens;
   const int32_t* pt = a.page_table + static_cast<size_t>(cd.slot) * a.max_pages;
-  const int h = g * G + wave;                                 // query head of this wave
+  const int h = g * G + wave % G;                             // query head of this wave
+  const int qblk = wave / G;                                  // query block (QT tiles of 32)
   const int n_q_heads = a.n_kv_heads * G;
   const size_t head_stride = static_cast<size_t>(2 * kPageTokens * D);
   const size_t layer_base = static_cast<size_t>(a.layer) * a.n_pages * a.n_kv_heads * head_stride +
                             static_cast<size_t>(g) * head_stride;
   const size_t page_stride = static_cast<size_t>(a.n_kv_heads) * head_stride;
+  const float c = a.scale_log2;
 
   // ---- global -> register staging of one K/V tile (pages 4j .. 4j+3) ------------------------
-  uint4 kreg[PER], vreg[PER];
-  auto load_tile = [&](int j) {
+  // Two register sets: the loads of tile j+2 are issued while tile j is computed and land in LDS
+  // at the end of tile j+1, so each load has two tile-iterations to arrive.
+  uint4 kregs[2][PER], vregs[2][PER];
+  auto load_tile = [&](int j, uint4 (&kreg)[PER], uint4 (&vreg)[PER]) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int i = tid + u * NT;
@@ -99,13 +112,13 @@ __global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
       }
     }
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf, const uint4 (&kreg)[PER], const uint4 (&vreg)[PER]) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int i = tid + u * NT;
       const int p = i / (2 * D), w = i % (2 * D);
-      const int row = kPageTokens * p + w / (D / 8), col = (w % (D / 8)) * 8;
-      st16(&sm.k[buf][row][col], kreg[u]);
+      const int row = kPageTokens * p + w / (D / 8), col8 = (w % (D / 8)) * 8;
+      st16(&sm.k[buf][row][col8], kreg[u]);
       const int dim = w >> 1, c0 = 2 * (w & 1);             // key groups c0, c0+1 of the page
       uint16_t* vrow = &sm.v[buf][dim][kPageTokens * p];
       st8(vrow + 4 * vt_group_pos(c0), make_uint2(vreg[u].x, vreg[u].y));
@@ -113,13 +126,13 @@ __global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
     }
   };
 
-  // ---- Q operand in registers: query q0 + 32*qt + lane%32, dims 16*ks + 8*(lane/32) ---------
+  // ---- Q operand in registers: query q0 + 32*(QT*qblk + qt) + lane%32, dims 16ks + 8*(lane/32)
   const int half = lane >> 5, col = lane & 31;
-  bf16x8 qop[2][KS];
-  int qpos[2];
+  bf16x8 qop[QT][KS];
+  int qpos[QT];
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
-    const int qi = tile.q0 + 32 * qt + col;
+  for (int qt = 0; qt < QT; ++qt) {
+    const int qi = tile.q0 + 32 * (QT * qblk + qt) + col;
     const bool valid = qi < cd.q_len;
     qpos[qt] = prefix + (valid ? qi : cd.q_len - 1);
     const uint16_t* qrow = a.q + (static_cast<size_t>(cd.q_row + (valid ? qi : 0)) * n_q_heads + h) * D;
@@ -128,29 +141,36 @@ __global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
       qop[qt][ks] = valid ? as_bf16x8(ld16(qrow + 16 * ks + 8 * half)) : bf16x8{};
   }
 
-  f32x16 o[DT][2];
+  f32x16 o[DT][QT];
 #pragma unroll
   for (int t = 0; t < DT; ++t)
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+    for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) o[t][qt][e] = 0.f;
-  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+  float m_s[QT], l_run[QT];   // running max (scaled, log2 units) and this lane's partial sum
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    m_s[qt] = -INFINITY;
+    l_run[qt] = 0.f;
+  }
+  const bf16x2 ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
 
-  load_tile(0);
-  store_tile(0);
+  load_tile(0, kregs[0], vregs[0]);
+  store_tile(0, kregs[0], vregs[0]);
+  if (n_kt > 1) load_tile(1, kregs[1], vregs[1]);
   __syncthreads();
 
-  for (int j = 0; j < n_kt; ++j) {
-    const int buf = j & 1;
-    if (j + 1 < n_kt) load_tile(j + 1);
+  auto tile_step = [&](const int j, const int buf, uint4 (&kl)[PER], uint4 (&vl)[PER],
+                       const uint4 (&ks_)[PER], const uint4 (&vs_)[PER]) {
+    if (j + 2 < n_kt) load_tile(j + 2, kl, vl);
 
-    // S^T tiles: [key subtile kt2][query tile qt]
-    f32x16 s[2][2];
+    // S^T tiles (raw scores): [key subtile kt2][query tile qt]
+    f32x16 s[2][QT];
 #pragma unroll
     for (int kt2 = 0; kt2 < 2; ++kt2)
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
+      for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) s[kt2][qt][e] = 0.f;
 #pragma unroll
@@ -159,37 +179,46 @@ __global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
       for (int kt2 = 0; kt2 < 2; ++kt2) {
         const bf16x8 kop = as_bf16x8(ld16(&sm.k[buf][32 * kt2 + col][16 * ks + 8 * half]));
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
+        for (int qt = 0; qt < QT; ++qt)
           s[kt2][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[qt][ks], s[kt2][qt], 0, 0, 0);
       }
     }
 
-    // Online softmax per query (one per lane and query tile).
+    // Online softmax, one query per lane and query tile; exp2 of c*s - m with c = log2(e)/sqrt(d).
     const bool need_mask = kBN * j + kBN - 1 > pos_min;
-    bf16x8 pop[2][2][2];  // [qt][kt2][j2]
+    bf16x8 pop[QT][2][2];  // [qt][kt2][j2]
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
+      if (need_mask) {
+#pragma unroll
+        for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int key = kBN * j + 32 * kt2 + 8 * (e >> 2) + 4 * half + (e & 3);
+            if (key > qpos[qt]) s[kt2][qt][e] = -INFINITY;
+          }
+      }
       float mx = -INFINITY;
 #pragma unroll
       for (int kt2 = 0; kt2 < 2; ++kt2)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = kBN * j + 32 * kt2 + 8 * (e >> 2) + 4 * half + (e & 3);
-          float x = s[kt2][qt][e] * a.scale_log2;
-          if (need_mask && key > qpos[qt]) x = -INFINITY;
-          s[kt2][qt][e] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, xor_shfl(mx, 32));
-      const float m_new = fmaxf(m_run[qt], mx);
-      const float alpha = fast_exp2(m_run[qt] - m_new);
-      m_run[qt] = m_new;
-      float psum = 0.f;
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt2][qt][e]);
+      mx = fmaxf(mx, xor_shfl(mx, 32)) * c;
+      if (__builtin_amdgcn_ballot_w64(mx > m_s[qt] + kRescaleLog2) != 0) {
+        const float m_new = fmaxf(m_s[qt], mx);
+        const float alpha = fast_exp2(m_s[qt] - m_new);
+        m_s[qt] = m_new;
+        l_run[qt] *= alpha;
+#pragma unroll
+        for (int t = 0; t < DT; ++t) o[t][qt] *= alpha;
+      }
+      const float neg_m = -m_s[qt];
+      float ps0 = 0.f, ps1 = 0.f;
 #pragma unroll
       for (int kt2 = 0; kt2 < 2; ++kt2) {
         float p[16];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) p[e] = fast_exp2(s[kt2][qt][e] - m_new);
+        for (int e = 0; e < 16; ++e) p[e] = fast_exp2(__builtin_fmaf(s[kt2][qt][e], c, neg_m));
 #pragma unroll
         for (int j2 = 0; j2 < 2; ++j2) {
           const uint4 pw = make_uint4(pack_bf16x2(p[8 * j2 + 0], p[8 * j2 + 1]),
@@ -197,13 +226,14 @@ __global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
                                       pack_bf16x2(p[8 * j2 + 4], p[8 * j2 + 5]),
                                       pack_bf16x2(p[8 * j2 + 6], p[8 * j2 + 7]));
           // the denominator sums the same bf16-rounded weights the PV product uses
-          psum += (sum_bf16x2(pw.x) + sum_bf16x2(pw.y)) + (sum_bf16x2(pw.z) + sum_bf16x2(pw.w));
+          ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw.x), ones, ps0, false);
+          ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw.y), ones, ps1, false);
+          ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw.z), ones, ps0, false);
+          ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw.w), ones, ps1, false);
           pop[qt][kt2][j2] = __builtin_bit_cast(bf16x8, pw);
         }
       }
-      l_run[qt] = l_run[qt] * alpha + psum;
-#pragma unroll
-      for (int t = 0; t < DT; ++t) o[t][qt] *= alpha;
+      l_run[qt] += ps0 + ps1;
     }
 
     // O^T += V^T . P^T over the 4 k-steps (16 keys each) of the tile.
@@ -216,18 +246,22 @@ __global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
           const bf16x8 vop =
               as_bf16x8(ld16(&sm.v[buf][32 * t + col][32 * kt2 + 16 * j2 + 8 * half]));
 #pragma unroll
-          for (int qt = 0; qt < 2; ++qt)
+          for (int qt = 0; qt < QT; ++qt)
             o[t][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[qt][kt2][j2], o[t][qt], 0, 0, 0);
         }
 
-    if (j + 1 < n_kt) store_tile(buf ^ 1);
+    if (j + 1 < n_kt) store_tile(buf ^ 1, ks_, vs_);
     __syncthreads();
+  };
+  for (int j = 0; j < n_kt; j += 2) {
+    tile_step(j, 0, kregs[0], vregs[0], kregs[1], vregs[1]);
+    if (j + 1 < n_kt) tile_step(j + 1, 1, kregs[1], vregs[1], kregs[0], vregs[0]);
   }
 
   // Normalise and write: lane owns query col of tile qt, dims 32t + 8(e/4) + 4*half + e%4.
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
-    const int qi = tile.q0 + 32 * qt + col;
+  for (int qt = 0; qt < QT; ++qt) {
+    const int qi = tile.q0 + 32 * (QT * qblk + qt) + col;
     const float l_tot = l_run[qt] + xor_shfl(l_run[qt], 32);
     if (qi >= cd.q_len) continue;
     const float inv = 1.f / l_tot;
@@ -245,7 +279,8 @@ __global__ __launch_bounds__(64 * G) void attn_fwd_kernel(ExtendArgs a) {
 
 template <int D, int G>
 static void launch_fwd(const ExtendArgs& a, int n_tiles, int n_kv_heads, hipStream_t stream) {
-  attn_fwd_kernel<D, G><<<n_tiles * n_kv_heads, 64 * G, 0, stream>>>(a);
+  constexpr int QT = D == 64 ? 2 : (G == 2 ? 1 : CS_FWD_QT);
+  attn_fwd_kernel<D, G, QT><<<n_tiles * n_kv_heads, 64 * G * (2 / QT), 0, stream>>>(a);
 }
 
 hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,
@@ -270,7 +305,7 @@ hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_c
     launch_fwd<DD, GG>(a, n_tiles, g.n_kv_heads, stream);     \
     return hipGetLastError();                                 \
   }
-  CS_FWD_CASE(128, 1) CS_FWD_CASE(128, 2) CS_FWD_CASE(128, 4) CS_FWD_CASE(128, 8)
+  CS_FWD_CASE(128, 2) CS_FWD_CASE(128, 4)
   CS_FWD_CASE(64, 1) CS_FWD_CASE(64, 2) CS_FWD_CASE(64, 4) CS_FWD_CASE(64, 8)
 #undef CS_FWD_CASE
   return hipErrorInvalidValue;
