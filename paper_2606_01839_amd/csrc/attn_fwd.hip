@@ -1,7 +1,8 @@
 // Turn-1 prefill and turn-N extend-prefill attention over paged KV (flash-attention forward).
 //
-// A workgroup owns one (conversation, 64-query block, kv head) tile; its G waves are the G query
-// heads of that kv head (the GQA group), so every K/V tile staged in LDS serves 64*G query rows.
+// A workgroup owns one (conversation, 64-query block, kv head) tile; its waves cover the G query
+// heads of that kv head (the GQA group) -- at head_dim 128 two waves per head, 32 queries each,
+// two waves per SIMD -- so every K/V tile staged in LDS serves 64*G query rows.
 // Each wave computes the transposed score tile on the matrix cores (v_mfma_f32_32x32x16_bf16):
 //   S^T[key][query] = K[key][:] . Q[query][:]       A = K rows from LDS, B = Q kept in registers
 //   O^T[dim][query] += V^T[dim][key] . P^T[key][query]   A = V^T rows from LDS, B = P registers
@@ -9,7 +10,8 @@
 // two 32-lane halves holding alternating groups of 4 keys), so the online-softmax max/sum are
 // in-lane except for one exchange between the halves, and the P accumulator registers are
 // directly the B operand of the PV product (the key order inside V^T is permuted in LDS to match).
-// K/V tiles of 64 keys (4 pages) are double-buffered in LDS; fully visible tiles skip the mask.
+// K/V tiles of 64 keys (4 pages) are double-buffered in LDS and their global loads are issued two
+// tiles ahead; fully visible tiles skip the mask.
 #include <cmath>
 
 #include "device_common.hpp"
@@ -47,17 +49,14 @@ struct FwdSmem {
 // as one 16-byte run.
 __device__ __forceinline__ int vt_group_pos(int c) { return ((c & 1) << 1) | (c >> 1); }
 
-#ifndef CS_FWD_QT
-#define CS_FWD_QT 1  // 32-query tiles per wave: 1 -> 2G waves per workgroup, 2 -> G waves
-#endif
-
 // Lazy rescaling threshold (log2 units): the running max used in the exponent is only raised when
 // a new score exceeds it by more than this, so P <= 2^8 and the O/l rescale is rare.
 constexpr float kRescaleLog2 = 8.f;
 
-template <int D, int G, int QT>
-__global__ __launch_bounds__(64 * G * (2 / QT)) void attn_fwd_kernel(ExtendArgs a) {
-  constexpr int NW = G * (2 / QT);     // waves: G query heads x (2 / QT) query blocks
+template <int D, int G, int QT, int BM>
+__global__ __launch_bounds__(64 * G * (BM / (32 * QT))) __attribute__((amdgpu_waves_per_eu(QT == 1 ? 2 : 1)))
+void attn_fwd_kernel(ExtendArgs a) {
+  constexpr int NW = G * (BM / (32 * QT));  // waves: G query heads x BM/(32 QT) query blocks
   constexpr int NT = 64 * NW;          // threads
   constexpr int KS = D / 16;           // k-steps of QK^T (16 dims each)
   constexpr int DT = D / 32;           // 32-dim output tiles
@@ -71,7 +70,7 @@ __global__ __launch_bounds__(64 * G * (2 / QT)) void attn_fwd_kernel(ExtendArgs 
   const ExtendTile tile = a.tiles[tile_idx];
   const ExtendConvDesc cd = a.convs[tile.conv];
   const int prefix = cd.len - cd.q_len;
-  const int q_hi = min(cd.q_len, tile.q0 + kBM);             // queries [q0, q_hi)
+  const int q_hi = min(cd.q_len, tile.q0 + BM);              // queries [q0, q_hi)
   const int pos_min = prefix + tile.q0, pos_max = prefix + q_hi - 1;
   const int n_kt = pos_max / kBN + 1;                        // key tiles 0 .. n_kt-1
   const int n_pg = (cd.len + kPageTokens - 1) / kPageTokens;
@@ -277,11 +276,15 @@ __global__ __launch_bounds__(64 * G * (2 / QT)) void attn_fwd_kernel(ExtendArgs 
   }
 }
 
+// head_dim 128: 32 queries per wave, 2G waves (two per SIMD at G = 4); head_dim 64: 64 queries
+// per wave, G waves.
 template <int D, int G>
 static void launch_fwd(const ExtendArgs& a, int n_tiles, int n_kv_heads, hipStream_t stream) {
-  constexpr int QT = D == 64 ? 2 : (G == 2 ? 1 : CS_FWD_QT);
-  attn_fwd_kernel<D, G, QT><<<n_tiles * n_kv_heads, 64 * G * (2 / QT), 0, stream>>>(a);
+  constexpr int QT = D == 64 ? 2 : 1;
+  attn_fwd_kernel<D, G, QT, kBM><<<n_tiles * n_kv_heads, 64 * G * (kBM / (32 * QT)), 0, stream>>>(a);
 }
+
+int extend_query_tile(int) { return kBM; }
 
 hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,
                          const ExtendTile* d_tiles, int n_tiles, const void* q, void* out,

@@ -304,7 +304,7 @@ cs_status attend(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* q_l
     slots[i] = cs::ConvTable::slot_of(convs[i]);
     lens[i] = cv[i]->len;
   }
-  cs::ExtendPlan plan = cs::plan_extend(slots, lens, ql, 64);
+  cs::ExtendPlan plan = cs::plan_extend(slots, lens, ql, cs::extend_query_tile(p->desc.head_dim));
   const size_t max_tiles =
       (kQuarter - align_up(plan.convs.size() * sizeof(cs::ExtendConvDesc), 16) - kAlign) /
       sizeof(cs::ExtendTile);
