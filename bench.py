@@ -31,8 +31,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 from synth import values as sv  # noqa: E402
-from synth.traces import (DecodeBatch, ExtendBatch, PrefillTransfer, KIND_K, KIND_Q,  # noqa: E402
-                          KIND_V, pages_for)
+from synth.traces import (DecodeBatch, ExtendBatch, MixedTrace, PrefillTransfer, KIND_K,  # noqa: E402
+                          KIND_Q, KIND_V, pages_for)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
@@ -332,6 +332,202 @@ def bench_prefill_transfer(args):
     }
 
 
+# ------------------------------------------------------------------------------------------------
+# mixed agentic trace (256 conversations, 32 layers, Llama-3-8B attention shape)
+# ------------------------------------------------------------------------------------------------
+class _Live:
+    __slots__ = ("tr", "h", "turn", "phase", "left", "length")
+
+    def __init__(self, tr, h, length):
+        self.tr, self.h, self.turn, self.length = tr, h, 0, length
+        self.phase, self.left = "decode", tr.decodes[0]
+
+
+def bench_mixed(args):
+    """Serve the synthetic agentic trace on one decoder pool for `args.mixed_steps` timed steps.
+
+    Admission is staggered: a conversation is admitted when the decoder pool's free pages cover its
+    (known, synthetic) final length. At admission its turn-1 prompt is prefilled on a separate
+    prefiller pool (all layers), packed, unpacked into the decoder pool and released from the
+    prefiller -- the one-time transfer. Every step, each live conversation either appends its
+    pending turn chunk (extend; whole chunks, at most 8192 extend tokens per step) or decodes one
+    token; finished conversations are destroyed and new ones admitted between steps."""
+    from paper_2606_01839_amd import KVPool
+    tr = MixedTrace()
+    sh = tr.shape
+    NL, hq, hkv, d = sh.n_layers, sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    trace = tr.conversations()
+    page_bytes = NL * hkv * 2 * 16 * d * 2                       # one page, all layers
+    free, _ = torch.cuda.mem_get_info()
+    max_t1 = max(c.turn1 for c in trace)
+    reserve = 3 * pages_for(max_t1) * page_bytes + (24 << 30)    # prefiller, wire, step buffers
+    n_pages = int((0.85 * free - reserve) // page_bytes)
+    max_final = max(c.final_len() for c in trace)
+    dec = KVPool(NL, hq, hkv, d, n_pages=n_pages, max_convs=tr.n_convs,
+                 max_pages_per_conv=pages_for(max_final), placement_seed=tr.seed + 1)
+    pre = KVPool(NL, hq, hkv, d, n_pages=pages_for(max_t1) + 16, max_convs=2,
+                 max_pages_per_conv=pages_for(max_t1) + 16, placement_seed=tr.seed + 2)
+    keys = {}
+
+    def key(c, kind, layer):
+        kk = keys.get((c, kind, layer))
+        if kk is None:
+            kk = keys[(c, kind, layer)] = sv.mix_key(tr.seed, c, kind, layer)
+        return kk
+
+    def rows(kind, items, layer, H, device="cuda"):
+        """Values of tokens (conv, start, n) for one layer: [sum n][H][d]."""
+        klist = np.array([sv.signed_key(key(c, kind, layer)) for c, _, _ in items], dtype=np.int64)
+        kk = np.repeat(klist, [n for _, _, n in items])
+        st = np.concatenate([(p0 + np.arange(n, dtype=np.int64)) * H * d for _, p0, n in items])
+        return sv.bf16_rows(kk, st, H * d, device=device).view(-1, H, d)
+
+    stats = {"prefill_flops": 0, "prefill_ms": 0.0, "pack_ms": 0.0, "unpack_ms": 0.0, "move_bytes": 0,
+             "admitted": 0, "completed": 0}
+    live, queue = [], list(trace)
+    reserved = [0]
+
+    def admit():
+        while queue and reserved[0] + pages_for(queue[0].final_len()) <= n_pages:
+            c = queue.pop(0)
+            L = c.turn1
+            h = pre.conv_create()
+            k = torch.stack([rows(KIND_K, [(c.cid, 0, L)], l, hkv) for l in range(NL)])
+            v = torch.stack([rows(KIND_V, [(c.cid, 0, L)], l, hkv) for l in range(NL)])
+            pre.kv_append(h, k, v)
+            del k, v
+            qs = [rows(KIND_Q, [(c.cid, 0, L)], l, hq) for l in range(NL)]
+            out = torch.empty_like(qs[0])
+            torch.cuda.synchronize()
+            pre.profile_start()
+            for l in range(NL):
+                pre.attn_prefill_turn1([h], [L], l, qs[l], out)
+            wire = pre.kv_pack(h)
+            pp = pre.profile_stop()
+            dec.profile_start()
+            hd = dec.kv_unpack(wire, L)
+            up = dec.profile_stop()
+            pre.conv_destroy(h)
+            del qs, out, wire
+            stats["prefill_ms"] += pp["attn_fwd"][0]
+            stats["pack_ms"] += pp["pack"][0]
+            stats["unpack_ms"] += up["unpack"][0]
+            stats["prefill_flops"] += attn_flops([0], [L], hq, d) * NL
+            stats["move_bytes"] += 2 * L * NL * hkv * d * 2 * 2
+            stats["admitted"] += 1
+            reserved[0] += pages_for(c.final_len())
+            live.append(_Live(c, hd, L))
+
+    t0 = time.perf_counter()
+    admit()
+    log(f"mixed: decoder pool {n_pages} pages; admitted {len(live)} conversations "
+        f"in {time.perf_counter() - t0:.1f}s")
+    tot = {"wall_s": 0.0, "tokens": 0, "dec_bytes": 0, "ext_flops": 0, "split_ms": 0.0, "merge_ms": 0.0,
+           "fwd_ms": 0.0, "append_ms": 0.0, "append_bytes": 0, "steps": 0, "dec_tokens": 0, "ext_tokens": 0}
+    parity = None
+    for step in range(args.mixed_steps + 1):
+        ext, budget = [], 8192
+        for lc in live:
+            if lc.phase == "append":
+                n = lc.tr.appends[lc.turn - 1]
+                if not ext or sum(x[1] for x in ext) + n <= budget:
+                    ext.append((lc, n))
+        dcs = [lc for lc in live if lc.phase == "decode"]
+        items_new = [(lc.tr.cid, lc.length, n) for lc, n in ext] + [(lc.tr.cid, lc.length, 1) for lc in dcs]
+        k = torch.stack([rows(KIND_K, items_new, l, hkv) for l in range(NL)])
+        v = torch.stack([rows(KIND_V, items_new, l, hkv) for l in range(NL)])
+        qe = torch.stack([rows(KIND_Q, items_new[:len(ext)], l, hq) for l in range(NL)]) if ext else None
+        qd = torch.stack([rows(KIND_Q, items_new[len(ext):], l, hq) for l in range(NL)]) if dcs else None
+        torch.cuda.synchronize()
+        timed_step = step > 0                                      # step 0 warms up
+        if timed_step:
+            dec.profile_start()
+        ts = time.perf_counter()
+        oe, od = dec.mixed_step([lc.h for lc, _ in ext], [n for _, n in ext], [lc.h for lc in dcs], k, v, qe, qd)
+        torch.cuda.synchronize()
+        te = time.perf_counter()
+        if timed_step:
+            pr = dec.profile_stop()
+            n_ext = sum(n for _, n in ext)
+            tot["wall_s"] += te - ts
+            tot["tokens"] += n_ext + len(dcs)
+            tot["ext_tokens"] += n_ext
+            tot["dec_tokens"] += len(dcs)
+            tot["dec_bytes"] += NL * (sum(lc.length + 1 for lc in dcs) * 2 * hkv * d * 2
+                                      + 2 * len(dcs) * hq * d * 2
+                                      + sum(pages_for(lc.length + 1) for lc in dcs) * 4)
+            tot["ext_flops"] += NL * attn_flops([lc.length for lc, _ in ext], [n for _, n in ext], hq, d)
+            tot["split_ms"] += pr["decode_split"][0]
+            tot["merge_ms"] += pr["decode_merge"][0]
+            tot["fwd_ms"] += pr["attn_fwd"][0]
+            tot["append_ms"] += pr["append"][0]
+            tot["append_bytes"] += 2 * NL * (n_ext + len(dcs)) * hkv * d * 2 * 2
+            tot["steps"] += 1
+        if parity is None and dcs and ext:
+            # spot check: shortest decoding and shortest extending conversation, first and last layer
+            from oracle.attention import attend_rows
+            errs = []
+            lcd = min(dcs, key=lambda x: x.length)
+            i_d = dcs.index(lcd)
+            i_e = min(range(len(ext)), key=lambda i: ext[i][0].length)
+            lce, ne = ext[i_e]
+            row_e = sum(n for _, n in ext[:i_e + 1]) - 1
+            for layer in (0, NL - 1):
+                for lc, qrow, outrow, pos in ((lcd, qd[layer, i_d], od[layer, i_d], lcd.length),
+                                              (lce, qe[layer, row_e], oe[layer, row_e], lce.length + ne - 1)):
+                    kk = rows(KIND_K, [(lc.tr.cid, 0, pos + 1)], layer, hkv, device="cpu")
+                    vv = rows(KIND_V, [(lc.tr.cid, 0, pos + 1)], layer, hkv, device="cpu")
+                    ref = attend_rows(sv.bf16_to_f64(qrow[None]), [pos], sv.bf16_to_f64(kk), sv.bf16_to_f64(vv))
+                    errs.append(float(np.abs(sv.bf16_to_f64(outrow[None]) - ref).max()))
+            parity = {"samples": len(errs), "max_abs": max(errs), "ok": bool(max(errs) <= 1e-2)}
+        del k, v, qe, qd, oe, od
+        # advance the trace
+        for lc, n in ext:
+            lc.length += n
+            lc.phase, lc.left = "decode", lc.tr.decodes[lc.turn]
+        finished = []
+        for lc in dcs:
+            lc.length += 1
+            lc.left -= 1
+            if lc.left == 0:
+                lc.turn += 1
+                if lc.turn == lc.tr.turns:
+                    finished.append(lc)
+                else:
+                    lc.phase = "append"
+        for lc in finished:
+            live.remove(lc)
+            dec.conv_destroy(lc.h)
+            reserved[0] -= pages_for(lc.tr.final_len())
+            stats["completed"] += 1
+        if finished:
+            admit()
+    used, free_pages = dec.occupancy()
+    dec.close()
+    pre.close()
+    torch.cuda.empty_cache()
+    gbs = lambda b, ms: b / (ms * 1e-3) / 1e9 if ms > 0 else None
+    tfs = lambda f, ms: f / (ms * 1e-3) / 1e12 if ms > 0 else None
+    return {"mixed": {
+        "workload": f"mixed agentic trace: {tr.n_convs} conversations, turns U[{tr.turns_lo},{tr.turns_hi}], "
+                    f"turn-1 logN(median {tr.turn1_median}) <= {tr.turn1_hi}, appends logN(median "
+                    f"{tr.append_median}), decodes logN(median {tr.decode_median}); {NL} layers "
+                    f"{hq}q/{hkv}kv d{d}; decoder pool {n_pages} pages ({n_pages * page_bytes / 2**30:.0f} GiB)",
+        "timed_steps": tot["steps"], "live_convs_end": len(live), "admitted": stats["admitted"],
+        "completed": stats["completed"], "tokens_per_s": tot["tokens"] / tot["wall_s"] if tot["wall_s"] else None,
+        "step_ms": 1e3 * tot["wall_s"] / max(1, tot["steps"]),
+        "decode_tokens": tot["dec_tokens"], "extend_tokens": tot["ext_tokens"],
+        "decode_gbs": gbs(tot["dec_bytes"], tot["split_ms"] + tot["merge_ms"]),
+        "decode_split_gbs": gbs(tot["dec_bytes"], tot["split_ms"]),
+        "extend_tflops": tfs(tot["ext_flops"], tot["fwd_ms"]),
+        "append_gbs": gbs(tot["append_bytes"], tot["append_ms"]),
+        "turn1_prefill_tflops": tfs(stats["prefill_flops"], stats["prefill_ms"]),
+        "pack_gbs": gbs(stats["move_bytes"], stats["pack_ms"]),
+        "unpack_gbs": gbs(stats["move_bytes"], stats["unpack_ms"]),
+        "occupancy_end": {"used_pages": used, "free_pages": free_pages},
+        "spot_parity": parity}}
+
+
 def copy_calibration():
     """A plain 1 GiB device copy: its FETCH_SIZE / WRITE_SIZE counters calibrate the HBM traffic
     reported for the decode kernel (known 1 GiB read + 1 GiB written)."""
@@ -348,6 +544,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--skip-components", action="store_true")
+    ap.add_argument("--mixed-steps", type=int, default=12,
+                    help="timed steps of the mixed agentic trace component (0 = skip it)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB copy (for counter calibration under rocprofv3)")
     args = ap.parse_args()
@@ -366,6 +564,8 @@ def main():
     if not args.skip_components:
         comps.update(bench_extend(args))
         comps.update(bench_prefill_transfer(args))
+        if args.mixed_steps > 0:
+            comps.update(bench_mixed(args))
     split_gbs = dec["split_bytes"] / (dec["split_ms"] * 1e-3) / 1e9
     line = {
         "metric": METRIC,

@@ -164,6 +164,25 @@ cs_status cs_attn_extend(cs_pool* pool, int32_t n_convs, const cs_conv* convs,
 cs_status cs_attn_decode_batch(cs_pool* pool, int32_t n_convs, const cs_conv* convs,
                                int32_t layer, const void* q, void* out, cs_stream stream);
 
+/*
+ * One step of a decoder serving agentic conversations (Section 4: after the one-time transfer a
+ * conversation's later turns -- incremental prefill of appended tokens and decoding -- run on its
+ * decoder; Section 2.1: dynamic batching lets requests join and leave every iteration). In one
+ * call: conversations ext_convs[i] append an extend chunk of ext_lens[i] >= 1 tokens and
+ * conversations dec_convs[j] append one decoded token (all layers), then for every layer the extend
+ * queries attend (as cs_attn_extend) and the decode queries attend (as cs_attn_decode_batch).
+ * All conversations must be distinct.
+ *   k, v:     [n_layers][sum(ext_lens) + n_dec][n_kv_heads][head_dim], extend tokens first
+ *   q_ext:    [n_layers][sum(ext_lens)][n_q_heads][head_dim];  out_ext same shape
+ *   q_dec:    [n_layers][n_dec][n_q_heads][head_dim];          out_dec same shape
+ * The batch metadata is uploaded once and reused by every layer's launches.
+ * Errors: as cs_kv_append_batch, cs_attn_extend and cs_attn_decode_batch.
+ */
+cs_status cs_mixed_step(cs_pool* pool, int32_t n_ext, const cs_conv* ext_convs,
+                        const int32_t* ext_lens, int32_t n_dec, const cs_conv* dec_convs,
+                        const void* k, const void* v, const void* q_ext, void* out_ext,
+                        const void* q_dec, void* out_dec, cs_stream stream);
+
 /* Wire size of a conversation's KV: n_layers * ceil(len/16) * n_kv_heads * 64 * head_dim bytes. */
 cs_status cs_kv_pack_size(const cs_pool* pool, cs_conv conv, size_t* bytes);
 

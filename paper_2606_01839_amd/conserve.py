@@ -24,7 +24,8 @@ EXPORTS = [
     "cs_pool_kv_bytes", "cs_pool_workspace_bytes", "cs_pool_create", "cs_pool_destroy",
     "cs_pool_occupancy", "cs_conv_create", "cs_conv_destroy", "cs_conv_len", "cs_conv_pages",
     "cs_kv_append", "cs_kv_append_batch", "cs_attn_prefill_turn1", "cs_attn_extend",
-    "cs_attn_decode_batch", "cs_kv_pack_size", "cs_kv_pack", "cs_kv_unpack", "cs_profile_start",
+    "cs_attn_decode_batch", "cs_mixed_step", "cs_kv_pack_size", "cs_kv_pack", "cs_kv_unpack",
+    "cs_profile_start",
     "cs_profile_stop", "cs_last_error",
 ]
 PROFILE_KINDS = ["append", "pack", "unpack", "decode_split", "decode_merge", "attn_fwd"]
@@ -73,6 +74,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "cs_attn_prefill_turn1": (I32, [P, I32, PI32, PI32, I32, VP, VP, VP]),
         "cs_attn_extend": (I32, [P, I32, PI32, PI32, I32, VP, VP, VP]),
         "cs_attn_decode_batch": (I32, [P, I32, PI32, I32, VP, VP, VP]),
+        "cs_mixed_step": (I32, [P, I32, PI32, PI32, I32, PI32, VP, VP, VP, VP, VP, VP, VP]),
         "cs_kv_pack_size": (I32, [P, I32, ctypes.POINTER(SZ)]),
         "cs_kv_pack": (I32, [P, I32, VP, SZ, VP]),
         "cs_kv_unpack": (I32, [P, VP, SZ, I64, PI32, VP]),
@@ -258,6 +260,35 @@ class KVPool:
         _check(self.lib.cs_attn_decode_batch(self._handle, ca.size, cp, layer, qptr, optr,
                                              _stream_handle(self.device)))
         return out
+
+    def mixed_step(self, ext_convs, ext_lens, dec_convs, k, v, q_ext=None, q_dec=None,
+                   out_ext=None, out_dec=None):
+        """One decoder step: extend chunks + one decoded token per decoding conversation, appended
+        for every layer, then attention of every layer. Returns (out_ext, out_dec)."""
+        ea, ep = _i32_array(ext_convs)
+        la, lp = _i32_array(ext_lens)
+        da, dp = _i32_array(dec_convs)
+        if ea.size != la.size:
+            raise ValueError("ext_convs and ext_lens differ in length")
+        ne, nd, L = int(la.sum()), da.size, self.n_layers
+        kv_shape = (L, ne + nd, self.n_kv_heads, self.head_dim)
+        kp, vp = self._dev(k, "k", kv_shape), self._dev(v, "v", kv_shape)
+        eshape = (L, ne, self.n_q_heads, self.head_dim)
+        dshape = (L, nd, self.n_q_heads, self.head_dim)
+        qe = qd = oe = od = None
+        if ne:
+            qe = self._dev(q_ext, "q_ext", eshape)
+            if out_ext is None:
+                out_ext = torch.empty(eshape, dtype=torch.bfloat16, device=self.device)
+            oe = self._dev(out_ext, "out_ext", eshape)
+        if nd:
+            qd = self._dev(q_dec, "q_dec", dshape)
+            if out_dec is None:
+                out_dec = torch.empty(dshape, dtype=torch.bfloat16, device=self.device)
+            od = self._dev(out_dec, "out_dec", dshape)
+        _check(self.lib.cs_mixed_step(self._handle, ea.size, ep, lp, nd, dp, kp, vp, qe, oe, qd, od,
+                                      _stream_handle(self.device)))
+        return out_ext, out_dec
 
     # -- instrumentation -----------------------------------------------------------------------
     def profile_start(self) -> None:

@@ -274,6 +274,76 @@ size_t wire_size(const cs_pool_desc& d, int64_t len) {
 
 hipStream_t as_stream(cs_stream s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Extend/prefill work uploaded once and launchable for any layer.
+struct ExtendWork {
+  struct Part {
+    cs::ExtendConvDesc* convs;
+    cs::ExtendTile* tiles;
+    int n_tiles;
+  };
+  std::vector<Part> parts;
+};
+
+cs_status upload_extend(cs_pool* p, const std::vector<int32_t>& slots, const std::vector<int64_t>& lens,
+                        const std::vector<int32_t>& q_lens, ExtendWork* w) {
+  cs::ExtendPlan plan = cs::plan_extend(slots, lens, q_lens, cs::extend_query_tile(p->desc.head_dim));
+  const size_t desc_bytes = align_up(plan.convs.size() * sizeof(cs::ExtendConvDesc), 16);
+  if (desc_bytes + kAlign + sizeof(cs::ExtendTile) > kQuarter)
+    return fail(CS_ENOMEM, "batch descriptor exceeds the metadata ring");
+  const size_t max_tiles = (kQuarter - desc_bytes - kAlign) / sizeof(cs::ExtendTile);
+  for (size_t t0 = 0; t0 < plan.tiles.size(); t0 += max_tiles) {
+    const size_t t1 = std::min(plan.tiles.size(), t0 + max_tiles);
+    std::vector<cs::ExtendTile> part(plan.tiles.begin() + t0, plan.tiles.begin() + t1);
+    ExtendWork::Part pw{nullptr, nullptr, static_cast<int>(part.size())};
+    cs_status st = upload2(p, plan.convs, part, &pw.convs, &pw.tiles);
+    if (st != CS_OK) return st;
+    w->parts.push_back(pw);
+  }
+  return CS_OK;
+}
+
+cs_status launch_extend_layer(cs_pool* p, const ExtendWork& w, int layer, const void* q, void* out) {
+  const cs::PoolGeom g = p->geom();
+  for (const auto& pw : w.parts) {
+    cs_status st = timed_launch(p, CS_PROF_ATTN_FWD, "attention launch", [&] {
+      return cs::launch_extend(g, layer, pw.convs, pw.tiles, pw.n_tiles, q, out, p->stream);
+    });
+    if (st != CS_OK) return st;
+  }
+  return CS_OK;
+}
+
+struct DecodeWork {
+  cs::DecodeConvDesc* convs = nullptr;
+  int n_convs = 0, n_items = 0, split = 0;
+};
+
+cs_status upload_decode(cs_pool* p, const std::vector<int32_t>& slots, const std::vector<int64_t>& lens,
+                        DecodeWork* w) {
+  cs::DecodePlan plan = cs::plan_decode(slots, lens, p->desc.n_kv_heads, kDecodeTargetItems);
+  if (plan.n_items > max_decode_items(p->desc)) return fail(CS_ENOMEM, "decode partials exceed the workspace");
+  void* d = nullptr;
+  cs_status st = upload(p, plan.convs.data(), plan.convs.size() * sizeof(cs::DecodeConvDesc), &d);
+  if (st != CS_OK) return st;
+  w->convs = static_cast<cs::DecodeConvDesc*>(d);
+  w->n_convs = static_cast<int>(plan.convs.size());
+  w->n_items = plan.n_items;
+  w->split = plan.split_tokens;
+  return CS_OK;
+}
+
+cs_status launch_decode_layer(cs_pool* p, const DecodeWork& w, int layer, const void* q, void* out) {
+  const cs::PoolGeom g = p->geom();
+  cs_status st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
+    return cs::launch_decode_split(g, layer, w.convs, w.n_convs, w.n_items, w.split, q, p->partials(),
+                                   p->stream);
+  });
+  if (st != CS_OK) return st;
+  return timed_launch(p, CS_PROF_DECODE_MERGE, "decode merge launch", [&] {
+    return cs::launch_decode_merge(g, w.convs, w.n_convs, p->partials(), out, p->stream);
+  });
+}
+
 cs_status attend(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* q_lens, int32_t layer,
                  const void* q, void* out, cs_stream stream, bool turn1) {
   if (!p) return fail(CS_EINVAL, "null pool");
@@ -304,23 +374,9 @@ cs_status attend(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* q_l
     slots[i] = cs::ConvTable::slot_of(convs[i]);
     lens[i] = cv[i]->len;
   }
-  cs::ExtendPlan plan = cs::plan_extend(slots, lens, ql, cs::extend_query_tile(p->desc.head_dim));
-  const size_t max_tiles =
-      (kQuarter - align_up(plan.convs.size() * sizeof(cs::ExtendConvDesc), 16) - kAlign) /
-      sizeof(cs::ExtendTile);
-  const cs::PoolGeom g = p->geom();
-  for (size_t t0 = 0; t0 < plan.tiles.size(); t0 += max_tiles) {
-    const size_t t1 = std::min(plan.tiles.size(), t0 + max_tiles);
-    std::vector<cs::ExtendTile> part(plan.tiles.begin() + t0, plan.tiles.begin() + t1);
-    cs::ExtendConvDesc* dc = nullptr;
-    cs::ExtendTile* dt = nullptr;
-    if ((st = upload2(p, plan.convs, part, &dc, &dt)) != CS_OK) return st;
-    st = timed_launch(p, CS_PROF_ATTN_FWD, "attention launch", [&] {
-      return cs::launch_extend(g, layer, dc, dt, static_cast<int>(part.size()), q, out, p->stream);
-    });
-    if (st != CS_OK) return st;
-  }
-  return CS_OK;
+  ExtendWork w;
+  if ((st = upload_extend(p, slots, lens, ql, &w)) != CS_OK) return st;
+  return launch_extend_layer(p, w, layer, q, out);
 }
 
 cs_status append_impl(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* n_new,
@@ -508,22 +564,9 @@ cs_status cs_attn_decode_batch(cs_pool* p, int32_t n, const cs_conv* convs, int3
     slots[i] = cs::ConvTable::slot_of(convs[i]);
     lens[i] = cv[i]->len;
   }
-  cs::DecodePlan plan = cs::plan_decode(slots, lens, p->desc.n_kv_heads, kDecodeTargetItems);
-  if (plan.n_items > max_decode_items(p->desc))
-    return fail(CS_ENOMEM, "decode partials exceed the workspace");
-  void* d = nullptr;
-  if ((st = upload(p, plan.convs.data(), plan.convs.size() * sizeof(cs::DecodeConvDesc), &d)) != CS_OK)
-    return st;
-  const cs::PoolGeom g = p->geom();
-  const auto* dc = static_cast<const cs::DecodeConvDesc*>(d);
-  st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
-    return cs::launch_decode_split(g, layer, dc, n, plan.n_items, plan.split_tokens, q, p->partials(),
-                                   p->stream);
-  });
-  if (st != CS_OK) return st;
-  return timed_launch(p, CS_PROF_DECODE_MERGE, "decode merge launch", [&] {
-    return cs::launch_decode_merge(g, dc, n, p->partials(), out, p->stream);
-  });
+  DecodeWork w;
+  if ((st = upload_decode(p, slots, lens, &w)) != CS_OK) return st;
+  return launch_decode_layer(p, w, layer, q, out);
 }
 
 cs_status cs_kv_pack_size(const cs_pool* p, cs_conv conv, size_t* bytes) {
@@ -580,6 +623,71 @@ cs_status cs_kv_unpack(cs_pool* p, const void* src, size_t src_bytes, int64_t n_
                                n_tokens, static_cast<int>(p0), static_cast<int>(p1 - p0), p->stream);
     });
     if (st != CS_OK) return st;
+  }
+  return CS_OK;
+}
+
+cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, const int32_t* ext_lens,
+                        int32_t n_dec, const cs_conv* dec_convs, const void* k, const void* v,
+                        const void* q_ext, void* out_ext, const void* q_dec, void* out_dec,
+                        cs_stream stream) {
+  if (!p) return fail(CS_EINVAL, "null pool");
+  if (n_ext < 0 || n_dec < 0) return fail(CS_EINVAL, "negative batch size");
+  if ((n_ext > 0 && (!ext_convs || !ext_lens)) || (n_dec > 0 && !dec_convs))
+    return fail(CS_EINVAL, "null conversation or length array");
+  std::vector<cs_conv> all;
+  if (n_ext > 0) all.assign(ext_convs, ext_convs + n_ext);
+  if (n_dec > 0) all.insert(all.end(), dec_convs, dec_convs + n_dec);
+  std::vector<const cs::Conv*> cv;
+  cs_status st = check_convs(p, static_cast<int32_t>(all.size()), all.data(), cv);
+  if (st != CS_OK) return st;
+  std::vector<int32_t> n_new;
+  int64_t ext_rows = 0;
+  for (int32_t i = 0; i < n_ext; ++i) {
+    if (ext_lens[i] < 1) return fail(CS_EINVAL, "an extend chunk must hold at least one token");
+    ext_rows += ext_lens[i];
+    n_new.push_back(ext_lens[i]);
+  }
+  if (ext_rows > INT32_MAX) return fail(CS_EINVAL, "too many extend tokens");
+  n_new.insert(n_new.end(), static_cast<size_t>(n_dec), 1);
+  if (all.empty()) return CS_OK;
+  if ((ext_rows > 0 && (!q_ext || !out_ext)) || (n_dec > 0 && (!q_dec || !out_dec)))
+    return fail(CS_EINVAL, "null q/out");
+  if (align_up(static_cast<size_t>(n_ext) * sizeof(cs::ExtendConvDesc), 16) + kAlign +
+              sizeof(cs::ExtendTile) > kQuarter ||
+      static_cast<size_t>(n_dec) * sizeof(cs::DecodeConvDesc) > kQuarter)
+    return fail(CS_ENOMEM, "batch descriptor exceeds the metadata ring");
+  // append every new token (all layers); validates capacity and commits the host metadata
+  if ((st = append_impl(p, static_cast<int32_t>(all.size()), all.data(), n_new.data(), k, v, stream)) != CS_OK)
+    return st;
+  std::vector<int32_t> e_slots(n_ext), d_slots(n_dec), e_q(n_new.begin(), n_new.begin() + n_ext);
+  std::vector<int64_t> e_lens(n_ext), d_lens(n_dec);
+  for (int32_t i = 0; i < n_ext; ++i) {
+    e_slots[i] = cs::ConvTable::slot_of(ext_convs[i]);
+    e_lens[i] = p->convs.find(ext_convs[i])->len;
+  }
+  for (int32_t i = 0; i < n_dec; ++i) {
+    d_slots[i] = cs::ConvTable::slot_of(dec_convs[i]);
+    d_lens[i] = p->convs.find(dec_convs[i])->len;
+  }
+  ExtendWork ew;
+  DecodeWork dw;
+  if (n_ext > 0 && (st = upload_extend(p, e_slots, e_lens, e_q, &ew)) != CS_OK) return st;
+  if (n_dec > 0 && (st = upload_decode(p, d_slots, d_lens, &dw)) != CS_OK) return st;
+  const size_t row_bytes = static_cast<size_t>(p->desc.n_q_heads) * p->desc.head_dim * 2;
+  for (int32_t layer = 0; layer < p->desc.n_layers; ++layer) {
+    if (n_ext > 0) {
+      const size_t off = static_cast<size_t>(layer) * static_cast<size_t>(ext_rows) * row_bytes;
+      if ((st = launch_extend_layer(p, ew, layer, static_cast<const char*>(q_ext) + off,
+                                    static_cast<char*>(out_ext) + off)) != CS_OK)
+        return st;
+    }
+    if (n_dec > 0) {
+      const size_t off = static_cast<size_t>(layer) * static_cast<size_t>(n_dec) * row_bytes;
+      if ((st = launch_decode_layer(p, dw, layer, static_cast<const char*>(q_dec) + off,
+                                    static_cast<char*>(out_dec) + off)) != CS_OK)
+        return st;
+    }
   }
   return CS_OK;
 }

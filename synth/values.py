@@ -35,6 +35,11 @@ INV_STD_F32 = float(np.float32(math.sqrt(3.0) / 65536.0))
 IH_MEAN = 2 * 65535  # mean of the sum of four uniform integers in [0, 65535]
 
 
+def signed_key(c: int) -> int:
+    """A 64-bit stream key as the int64 value with the same bits (for int64 key arrays)."""
+    return _s64(c)
+
+
 def _s64(c: int) -> int:
     """Unsigned 64-bit constant -> the int64 value with the same bits."""
     c &= _M64
@@ -113,6 +118,32 @@ def bf16_tensor(key: int, shape, head_scale=None, head_axis: int = -2, device="c
             x = x * hs[(e // inner) % nh]
         out[c0:c1] = _f32_to_bf16_bits_t(x).to(torch.int16)
     return out.view(torch.bfloat16).view(shape)
+
+
+def bf16_rows(keys, starts, row_len: int, device="cpu") -> torch.Tensor:
+    """[R][row_len] bf16: row r holds stream ``keys[r]`` elements ``starts[r] .. +row_len``.
+
+    ``keys``: 64-bit stream keys (Python ints), or an int64 numpy array of their signed bits.
+
+    Same values as ``bf16_tensor`` (unscaled) for the same key and element indices; lets one call
+    generate the rows of many conversations / layers at once."""
+    if not (isinstance(keys, np.ndarray) and keys.dtype == np.int64):   # int64 arrays: already signed
+        keys = np.asarray([_s64(int(k)) for k in keys], dtype=np.int64)
+    keys = torch.as_tensor(keys, device=device)
+    starts = torch.as_tensor(np.asarray(starts, dtype=np.int64), device=device)
+    R = keys.numel()
+    if R == 0:
+        return torch.empty((0, row_len), dtype=torch.bfloat16, device=device)
+    idx = starts[:, None] + torch.arange(row_len, dtype=torch.int64, device=device)[None, :]
+    x = idx * _s64(_GOLDEN) + keys[:, None]
+    x = x ^ _lsr(x, 30)
+    x = x * _s64(_C1)
+    x = x ^ _lsr(x, 27)
+    x = x * _s64(_C2)
+    h = x ^ _lsr(x, 31)
+    s = (h & 0xFFFF) + ((h >> 16) & 0xFFFF) + ((h >> 32) & 0xFFFF) + _lsr(h, 48)
+    f = (s - IH_MEAN).to(torch.float32) * INV_STD_F32
+    return _f32_to_bf16_bits_t(f).to(torch.int16).view(torch.bfloat16).view(R, row_len)
 
 
 # ----------------------------------------------------------------------------------------------

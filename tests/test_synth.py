@@ -68,3 +68,12 @@ def test_trace_shapes():
     assert all(len(c.appends) == c.turns - 1 for c in convs)
     # deterministic
     assert [c.turn1 for c in convs] == [c.turn1 for c in st.MixedTrace().conversations()]
+
+
+def test_row_batched_generation_matches_streams():
+    keys = [sv.mix_key(3, c, st.KIND_K, l) for c in range(3) for l in range(2)]
+    starts = [17 * 64 * i for i in range(6)]
+    rows = sv.bf16_rows(keys, starts, 64 * 5)
+    for r, (k, s0) in enumerate(zip(keys, starts)):
+        ref = sv.bf16_tensor(k, (5, 64), start=s0)
+        assert torch.equal(rows[r].view(5, 64), ref)
