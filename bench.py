@@ -110,11 +110,13 @@ def blas_threads() -> int:
 
 
 # ------------------------------------------------------------------------------------------------
-# headline: decode batch
+# workload construction (shared with tests/test_gpu_fullsize.py)
 # ------------------------------------------------------------------------------------------------
-def bench_decode(args):
+def make_decode_case(tr=None):
+    """Decode batch pool: every conversation's K/V appended; returns (pool, convs, lens,
+    [(k, v)] device inputs per conversation, q [B][Hq][d] for each last position)."""
     from paper_2606_01839_amd import KVPool
-    tr = DecodeBatch()
+    tr = tr or DecodeBatch()
     sh = tr.shape
     hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
     lens = tr.lengths().astype(np.int64)
@@ -123,7 +125,6 @@ def bench_decode(args):
     pool = KVPool(1, hq, hkv, d, n_pages=n_pages, max_convs=tr.batch,
                   max_pages_per_conv=pages_for(tr.hi), placement_seed=tr.seed + 1)
     convs, kv_dev = [], []
-    t0 = time.perf_counter()
     for b, L in enumerate(lens):
         c = pool.conv_create()
         k, v = gen_kv(tr.seed, b, 0, int(L), hkv, d, sk, svs)
@@ -131,6 +132,66 @@ def bench_decode(args):
         convs.append(c)
         kv_dev.append((k, v))
     q = torch.cat([gen_q(tr.seed, b, int(L) - 1, 1, hq, d) for b, L in enumerate(lens)])
+    return pool, convs, lens, kv_dev, q
+
+
+def make_extend_case(tr=None):
+    """Extend batch: prefixes appended; returns (pool, convs, prefix, chunk, k_new, v_new, q) with
+    the turn's new K/V ([1][sum chunk][Hkv][d], not yet appended) and q [sum chunk][Hq][d]."""
+    from paper_2606_01839_amd import KVPool
+    tr = tr or ExtendBatch()
+    sh = tr.shape
+    hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    prefix, chunk = tr.lengths()
+    total = prefix + chunk
+    pool = KVPool(1, hq, hkv, d, n_pages=int(sum(pages_for(L) for L in total)) + 64,
+                  max_convs=tr.n_convs, max_pages_per_conv=pages_for(int(total.max())),
+                  placement_seed=tr.seed + 1)
+    convs = []
+    for b in range(tr.n_convs):
+        c = pool.conv_create()
+        k, v = gen_kv(tr.seed, b, 0, int(prefix[b]), hkv, d)
+        pool.kv_append(c, k[None], v[None])
+        convs.append(c)
+        del k, v
+    new_kv = [gen_kv(tr.seed, b, int(prefix[b]), int(chunk[b]), hkv, d) for b in range(tr.n_convs)]
+    kcat = torch.cat([k for k, _ in new_kv])[None].contiguous()
+    vcat = torch.cat([v for _, v in new_kv])[None].contiguous()
+    q = torch.cat([gen_q(tr.seed, b, int(prefix[b]), int(chunk[b]), hq, d) for b in range(tr.n_convs)])
+    return pool, convs, prefix, chunk, kcat, vcat, q
+
+
+def make_prefill_case(tr=None):
+    """Turn-1 prefill batch: prompts appended; returns (pool, convs, lens, q [sum L][Hq][d])."""
+    from paper_2606_01839_amd import KVPool
+    tr = tr or PrefillTransfer()
+    sh = tr.shape
+    hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    lens = tr.lengths().astype(np.int64)
+    npg = int(sum(pages_for(L) for L in lens)) + 64
+    pool = KVPool(1, hq, hkv, d, n_pages=npg, max_convs=tr.n_convs,
+                  max_pages_per_conv=pages_for(tr.hi), placement_seed=tr.seed + 1)
+    convs = []
+    for b, L in enumerate(lens):
+        c = pool.conv_create()
+        k, v = gen_kv(tr.seed, b, 0, int(L), hkv, d)
+        pool.kv_append(c, k[None], v[None])
+        convs.append(c)
+        del k, v
+    q = torch.cat([gen_q(tr.seed, b, 0, int(L), hq, d) for b, L in enumerate(lens)])
+    return pool, convs, lens, q
+
+
+# ------------------------------------------------------------------------------------------------
+# headline: decode batch
+# ------------------------------------------------------------------------------------------------
+def bench_decode(args):
+    tr = DecodeBatch()
+    sh = tr.shape
+    hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    t0 = time.perf_counter()
+    pool, convs, lens, kv_dev, q = make_decode_case(tr)
+    sk, svs = tr.head_scales()
     out = torch.empty_like(q)
     torch.cuda.synchronize()
     log(f"decode: filled {len(lens)} conversations ({lens.sum()} tokens) in {time.perf_counter() - t0:.1f}s")
@@ -204,31 +265,15 @@ def attn_flops(prefix, n, hq, d):
 
 
 def bench_extend(args):
-    from paper_2606_01839_amd import KVPool
     tr = ExtendBatch()
     sh = tr.shape
     hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
-    prefix, chunk = tr.lengths()
+    pool, convs, prefix, chunk, kcat, vcat, q = make_extend_case(tr)
     total = prefix + chunk
-    pool = KVPool(1, hq, hkv, d, n_pages=int(sum(pages_for(L) for L in total)) + 64,
-                  max_convs=tr.n_convs, max_pages_per_conv=pages_for(int(total.max())),
-                  placement_seed=tr.seed + 1)
-    convs = []
-    for b in range(tr.n_convs):
-        c = pool.conv_create()
-        k, v = gen_kv(tr.seed, b, 0, int(prefix[b]), hkv, d)
-        pool.kv_append(c, k[None], v[None])
-        convs.append(c)
-        del k, v
-    # the turn's new tokens are appended (timed separately), then attend
-    new_kv = [gen_kv(tr.seed, b, int(prefix[b]), int(chunk[b]), hkv, d) for b in range(tr.n_convs)]
-    kcat = torch.cat([k for k, _ in new_kv])[None].contiguous()
-    vcat = torch.cat([v for _, v in new_kv])[None].contiguous()
     torch.cuda.synchronize()
     pool.profile_start()
     pool.kv_append_batch(convs, chunk, kcat, vcat)
     app = pool.profile_stop()["append"]
-    q = torch.cat([gen_q(tr.seed, b, int(prefix[b]), int(chunk[b]), hq, d) for b in range(tr.n_convs)])
     out = torch.empty_like(q)
     step = lambda: pool.attn_extend(convs, chunk, 0, q, out)
     reps = max(3, args.steps // 4)
@@ -248,7 +293,7 @@ def bench_extend(args):
         err = np.abs(sv.bf16_to_f64(out[row:row + 1]) - ref).max()
         ok = ok and err <= 1e-2
     pool.close()
-    del new_kv, kcat, vcat
+    del kcat, vcat
     torch.cuda.empty_cache()
     return {
         "extend": {"workload": f"extend-prefill: {tr.n_convs} conversations, prefix U[{tr.prefix_lo},"
@@ -274,19 +319,10 @@ def bench_prefill_transfer(args):
     tr = PrefillTransfer()
     sh = tr.shape
     hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
-    lens = tr.lengths().astype(np.int64)
-    npg = int(sum(pages_for(L) for L in lens)) + 64
+    pre, convs, lens, q = make_prefill_case(tr)
+    npg = pre.desc.n_pages
     mk = lambda seed: KVPool(1, hq, hkv, d, n_pages=npg, max_convs=tr.n_convs,
                              max_pages_per_conv=pages_for(tr.hi), placement_seed=seed)
-    pre = mk(tr.seed + 1)
-    convs = []
-    for b, L in enumerate(lens):
-        c = pre.conv_create()
-        k, v = gen_kv(tr.seed, b, 0, int(L), hkv, d)
-        pre.kv_append(c, k[None], v[None])
-        convs.append(c)
-        del k, v
-    q = torch.cat([gen_q(tr.seed, b, 0, int(L), hq, d) for b, L in enumerate(lens)])
     out = torch.empty_like(q)
     step = lambda: pre.attn_prefill_turn1(convs, lens, 0, q, out)
     reps = 2
@@ -544,7 +580,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--skip-components", action="store_true")
-    ap.add_argument("--mixed-steps", type=int, default=12,
+    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed"], default=None,
+                    help="run one component and print only its JSON (for profiling)")
+    ap.add_argument("--mixed-steps", type=int, default=300,
                     help="timed steps of the mixed agentic trace component (0 = skip it)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB copy (for counter calibration under rocprofv3)")
@@ -559,9 +597,13 @@ def main():
     load_library()
     if args.calibrate_copy:
         copy_calibration()
+    if args.only and args.only != "decode":
+        fn = {"extend": bench_extend, "prefill": bench_prefill_transfer, "mixed": bench_mixed}[args.only]
+        print(json.dumps({"component": args.only, **fn(args)}), flush=True)
+        return
     dec = bench_decode(args)
     comps = {}
-    if not args.skip_components:
+    if not args.skip_components and not args.only:
         comps.update(bench_extend(args))
         comps.update(bench_prefill_transfer(args))
         if args.mixed_steps > 0:

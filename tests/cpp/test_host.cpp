@@ -1,0 +1,102 @@
+// Host-metadata unit test (page pool, conversation table, plans); built with -fsanitize=address,
+// undefined by tests/test_host_cpp.py. Exits non-zero on the first failed check.
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <set>
+#include <vector>
+
+#include "host/host_state.hpp"
+
+#define CHECK(c)                                                          \
+  do {                                                                    \
+    if (!(c)) {                                                           \
+      std::fprintf(stderr, "%s:%d: check failed: %s\n", __FILE__, __LINE__, #c); \
+      std::exit(1);                                                       \
+    }                                                                     \
+  } while (0)
+
+static void pool_basics() {
+  cs::PagePool a(100, 7), b(100, 7), c(100, 8);
+  std::vector<int32_t> pa, pb, pc;
+  CHECK(a.alloc(100, pa) && b.alloc(100, pb) && c.alloc(100, pc));
+  CHECK(pa == pb);                 // same seed, same placement
+  CHECK(pa != pc);                 // another seed, another placement
+  std::vector<int32_t> sorted = pa;
+  std::sort(sorted.begin(), sorted.end());
+  for (int i = 0; i < 100; ++i) CHECK(sorted[i] == i);  // a permutation of all pages
+  CHECK(a.free_count() == 0 && a.used_count() == 100);
+  std::vector<int32_t> more;
+  CHECK(!a.alloc(1, more) && more.empty());             // all-or-nothing
+  a.release(std::vector<int32_t>(pa.begin(), pa.begin() + 10));
+  CHECK(a.free_count() == 10);
+  CHECK(!a.alloc(11, more) && more.empty());
+  CHECK(a.alloc(10, more) && more.size() == 10);
+}
+
+static void conv_table() {
+  cs::PagePool pool(64, 1);
+  cs::ConvTable t(3, 8);
+  int32_t h[4];
+  CHECK(t.create(&h[0]) && t.create(&h[1]) && t.create(&h[2]));
+  CHECK(!t.create(&h[3]));
+  CHECK(t.find(h[1]) && t.live_count() == 3);
+  t.find(h[1])->len = 40;
+  CHECK(pool.alloc(3, t.find(h[1])->pages));
+  CHECK(pool.used_count() == 3);
+  t.destroy(h[1], pool);
+  CHECK(pool.used_count() == 0 && !t.find(h[1]) && t.live_count() == 2);
+  CHECK(t.create(&h[3]) && h[3] != h[1] && !t.find(h[1]));  // stale handle stays invalid
+  CHECK(cs::ConvTable::slot_of(h[3]) == cs::ConvTable::slot_of(h[1]));
+  CHECK(!t.find(-1) && !t.find(1 << 19));
+}
+
+static void decode_plan() {
+  std::vector<int32_t> slots = {4, 9, 2};
+  std::vector<int64_t> lens = {1, 1000, 4096};
+  cs::DecodePlan p = cs::plan_decode(slots, lens, 8, 1 << 30);  // unreachable target -> smallest split
+  CHECK(p.split_tokens == 128);
+  CHECK(p.convs.size() == 3 && p.convs[0].n_splits == 1 && p.convs[1].n_splits == 8 && p.convs[2].n_splits == 32);
+  CHECK(p.convs[1].item_start == 1 && p.convs[2].item_start == 9 && p.n_items == 41);
+  cs::DecodePlan q = cs::plan_decode(slots, lens, 8, 1);  // any split satisfies -> largest
+  CHECK(q.split_tokens == 1024 && q.n_items == 1 + 1 + 4);
+}
+
+static void extend_plan() {
+  std::vector<int32_t> slots = {0, 1};
+  std::vector<int64_t> lens = {100, 300};
+  std::vector<int32_t> ql = {100, 130};
+  cs::ExtendPlan p = cs::plan_extend(slots, lens, ql, 64);
+  CHECK(p.convs[0].q_row == 0 && p.convs[1].q_row == 100);
+  CHECK(p.tiles.size() == 2 + 3);
+  // longest first: conversation 1 (prefix 170) tile q0=128 sees 300 keys
+  CHECK(p.tiles[0].conv == 1 && p.tiles[0].q0 == 128);
+  std::set<std::pair<int, int>> seen;
+  for (auto& t : p.tiles) seen.insert({t.conv, t.q0});
+  CHECK(seen.size() == 5 && seen.count({0, 64}) && seen.count({1, 64}));
+}
+
+static void append_plan() {
+  std::vector<int32_t> pages0 = {7, 3};        // conversation with 20 tokens (2 pages) + 1 new
+  std::vector<int32_t> pages1 = {5};           // empty conversation receiving 16 tokens
+  std::vector<const std::vector<int32_t>*> lists = {&pages0, &pages1};
+  // conversation 0: tokens 20..49 -> page 1 slots 4..15, page 2 slots 0..15, page 3 slots 0..1
+  pages0.push_back(11);
+  pages0.push_back(12);
+  std::vector<cs::PageChunk> ch = cs::plan_append({2, 6}, {20, 0}, {30, 16}, lists);
+  CHECK(ch.size() == 3 + 1);
+  CHECK(ch[0].lpage == 1 && ch[0].page == 3 && ch[0].t0 == 4 && ch[0].t1 == 16 && ch[0].src_row == 0 && !ch[0].new_page);
+  CHECK(ch[1].lpage == 2 && ch[1].page == 11 && ch[1].t0 == 0 && ch[1].t1 == 16 && ch[1].src_row == 12 && ch[1].new_page);
+  CHECK(ch[2].lpage == 3 && ch[2].page == 12 && ch[2].t0 == 0 && ch[2].t1 == 2 && ch[2].src_row == 28 && ch[2].new_page);
+  CHECK(ch[3].conv == 1 && ch[3].lpage == 0 && ch[3].t0 == 0 && ch[3].t1 == 16 && ch[3].src_row == 30 && ch[3].new_page);
+}
+
+int main() {
+  pool_basics();
+  conv_table();
+  decode_plan();
+  extend_plan();
+  append_plan();
+  std::puts("host metadata tests passed");
+  return 0;
+}
