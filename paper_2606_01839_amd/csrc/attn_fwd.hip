@@ -172,16 +172,31 @@ void attn_fwd_kernel(ExtendArgs a) {
       for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) s[kt2][qt][e] = 0.f;
+    // All K operands of the tile are read from LDS before the first MFMA, so the LDS latency is
+    // paid once per tile instead of once per MFMA.
+    bf16x8 kop[KS][2];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int kt2 = 0; kt2 < 2; ++kt2) {
-        const bf16x8 kop = as_bf16x8(ld16(&sm.k[buf][32 * kt2 + col][16 * ks + 8 * half]));
+      for (int kt2 = 0; kt2 < 2; ++kt2)
+        kop[ks][kt2] = as_bf16x8(ld16(&sm.k[buf][32 * kt2 + col][16 * ks + 8 * half]));
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int kt2 = 0; kt2 < 2; ++kt2)
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt)
-          s[kt2][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[qt][ks], s[kt2][qt], 0, 0, 0);
-      }
-    }
+          s[kt2][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ks][kt2], qop[qt][ks], s[kt2][qt], 0, 0, 0);
+
+    // V operands are read now: their LDS latency overlaps the softmax below.
+    bf16x8 vop[2][2][DT];
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+      for (int j2 = 0; j2 < 2; ++j2)
+#pragma unroll
+        for (int t = 0; t < DT; ++t)
+          vop[kt2][j2][t] = as_bf16x8(ld16(&sm.v[buf][32 * t + col][32 * kt2 + 16 * j2 + 8 * half]));
 
     // Online softmax, one query per lane and query tile; exp2 of c*s - m with c = log2(e)/sqrt(d).
     const bool need_mask = kBN * j + kBN - 1 > pos_min;
@@ -202,7 +217,7 @@ void attn_fwd_kernel(ExtendArgs a) {
       for (int kt2 = 0; kt2 < 2; ++kt2)
 #pragma unroll
         for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt2][qt][e]);
-      mx = fmaxf(mx, xor_shfl(mx, 32)) * c;
+      mx = halves_max(mx) * c;
       if (__builtin_amdgcn_ballot_w64(mx > m_s[qt] + kRescaleLog2) != 0) {
         const float m_new = fmaxf(m_s[qt], mx);
         const float alpha = fast_exp2(m_s[qt] - m_new);
@@ -241,13 +256,10 @@ void attn_fwd_kernel(ExtendArgs a) {
 #pragma unroll
       for (int j2 = 0; j2 < 2; ++j2)
 #pragma unroll
-        for (int t = 0; t < DT; ++t) {
-          const bf16x8 vop =
-              as_bf16x8(ld16(&sm.v[buf][32 * t + col][32 * kt2 + 16 * j2 + 8 * half]));
+        for (int t = 0; t < DT; ++t)
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt)
-            o[t][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[qt][kt2][j2], o[t][qt], 0, 0, 0);
-        }
+            o[t][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[kt2][j2][t], pop[qt][kt2][j2], o[t][qt], 0, 0, 0);
 
     if (j + 1 < n_kt) store_tile(buf ^ 1, ks_, vs_);
     __syncthreads();
@@ -261,7 +273,7 @@ void attn_fwd_kernel(ExtendArgs a) {
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const int qi = tile.q0 + 32 * (QT * qblk + qt) + col;
-    const float l_tot = l_run[qt] + xor_shfl(l_run[qt], 32);
+    const float l_tot = halves_sum(l_run[qt]);
     if (qi >= cd.q_len) continue;
     const float inv = 1.f / l_tot;
     uint16_t* orow = a.out + (static_cast<size_t>(cd.q_row + qi) * n_q_heads + h) * D;
