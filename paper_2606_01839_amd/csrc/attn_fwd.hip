@@ -11,7 +11,8 @@
 // in-lane except for one exchange between the halves, and the P accumulator registers are
 // directly the B operand of the PV product (the key order inside V^T is permuted in LDS to match).
 // K/V tiles of 64 keys (4 pages) are double-buffered in LDS and their global loads are issued two
-// tiles ahead; fully visible tiles skip the mask.
+// tiles ahead (page ids through scalar loads, no branches around the loads, so the compiler's
+// vector-memory waits only ever wait for the older tile); fully visible tiles skip the mask.
 #include <cmath>
 
 #include "device_common.hpp"
@@ -88,40 +89,44 @@ void attn_fwd_kernel(ExtendArgs a) {
   // Two register sets: the loads of tile j+2 are issued while tile j is computed and land in LDS
   // at the end of tile j+1, so each load has two tile-iterations to arrive.
   uint4 kregs[2][PER], vregs[2][PER];
+  // A wave's 64 consecutive chunks always lie in one page, so the page id is wave-uniform and is
+  // read with a scalar load: the vector-memory counter then only tracks K/V data, and waiting for
+  // a page id never drains K/V loads still in flight for an earlier tile.
+  const __attribute__((address_space(4))) int32_t* ptc =
+      (const __attribute__((address_space(4))) int32_t*)reinterpret_cast<uintptr_t>(pt);
   auto load_tile = [&](int j, uint4 (&kreg)[PER], uint4 (&vreg)[PER]) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int i = tid + u * NT;
-      const int p = i / (2 * D);                 // page within tile (2D chunks per page)
-      const int lp = 4 * j + p;
-      kreg[u] = make_uint4(0, 0, 0, 0);
-      vreg[u] = make_uint4(0, 0, 0, 0);
-      if (lp < n_pg) {
-        const uint16_t* blk = a.pool + layer_base + static_cast<size_t>(pt[lp]) * page_stride;
-        const int w = i % (2 * D);
-        kreg[u] = ld16(blk + w * 8);                        // K: row w/(D/8), chunk w%(D/8)
-        vreg[u] = ld16(blk + kPageTokens * D + w * 8);      // V^T: dim w/2, keys 8*(w%2)..+8
-        const int key0 = kBN * j + kPageTokens * p + 8 * (w & 1);
-        if (key0 + 8 > cd.len) {                            // zero V of keys past the end
-          vreg[u].x = mask_bf16x2(vreg[u].x, key0 + 0 < cd.len, key0 + 1 < cd.len);
-          vreg[u].y = mask_bf16x2(vreg[u].y, key0 + 2 < cd.len, key0 + 3 < cd.len);
-          vreg[u].z = mask_bf16x2(vreg[u].z, key0 + 4 < cd.len, key0 + 5 < cd.len);
-          vreg[u].w = mask_bf16x2(vreg[u].w, key0 + 6 < cd.len, key0 + 7 < cd.len);
-        }
-      }
+      // Always load (pages past the end are clamped to the last page and zeroed when stored), so
+      // the number of loads in flight is the same on every path and the waits stay precise.
+      const int lp = min(__builtin_amdgcn_readfirstlane(4 * j + i / (2 * D)), n_pg - 1);
+      const int w = i % (2 * D);
+      const uint16_t* blk = a.pool + layer_base + static_cast<size_t>(ptc[lp]) * page_stride;
+      kreg[u] = ld16(blk + w * 8);                          // K: row w/(D/8), chunk w%(D/8)
+      vreg[u] = ld16(blk + kPageTokens * D + w * 8);        // V^T: dim w/2, keys 8*(w%2)..+8
     }
   };
-  auto store_tile = [&](int buf, const uint4 (&kreg)[PER], const uint4 (&vreg)[PER]) {
+  auto store_tile = [&](int buf, int j, const uint4 (&kreg)[PER], const uint4 (&vreg)[PER]) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int i = tid + u * NT;
       const int p = i / (2 * D), w = i % (2 * D);
       const int row = kPageTokens * p + w / (D / 8), col8 = (w % (D / 8)) * 8;
-      st16(&sm.k[buf][row][col8], kreg[u]);
+      const bool in_conv = 4 * j + p < n_pg;
+      st16(&sm.k[buf][row][col8], in_conv ? kreg[u] : make_uint4(0, 0, 0, 0));
+      uint4 vx = vreg[u];
+      const int key0 = kBN * j + kPageTokens * p + 8 * (w & 1);
+      if (key0 + 8 > cd.len) {                              // zero V of keys past the end
+        vx.x = mask_bf16x2(vx.x, key0 + 0 < cd.len, key0 + 1 < cd.len);
+        vx.y = mask_bf16x2(vx.y, key0 + 2 < cd.len, key0 + 3 < cd.len);
+        vx.z = mask_bf16x2(vx.z, key0 + 4 < cd.len, key0 + 5 < cd.len);
+        vx.w = mask_bf16x2(vx.w, key0 + 6 < cd.len, key0 + 7 < cd.len);
+      }
       const int dim = w >> 1, c0 = 2 * (w & 1);             // key groups c0, c0+1 of the page
       uint16_t* vrow = &sm.v[buf][dim][kPageTokens * p];
-      st8(vrow + 4 * vt_group_pos(c0), make_uint2(vreg[u].x, vreg[u].y));
-      st8(vrow + 4 * vt_group_pos(c0 + 1), make_uint2(vreg[u].z, vreg[u].w));
+      st8(vrow + 4 * vt_group_pos(c0), make_uint2(vx.x, vx.y));
+      st8(vrow + 4 * vt_group_pos(c0 + 1), make_uint2(vx.z, vx.w));
     }
   };
 
@@ -156,13 +161,13 @@ void attn_fwd_kernel(ExtendArgs a) {
   const bf16x2 ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
 
   load_tile(0, kregs[0], vregs[0]);
-  store_tile(0, kregs[0], vregs[0]);
-  if (n_kt > 1) load_tile(1, kregs[1], vregs[1]);
+  store_tile(0, 0, kregs[0], vregs[0]);
+  load_tile(min(1, n_kt - 1), kregs[1], vregs[1]);
   __syncthreads();
 
   auto tile_step = [&](const int j, const int buf, uint4 (&kl)[PER], uint4 (&vl)[PER],
                        const uint4 (&ks_)[PER], const uint4 (&vs_)[PER]) {
-    if (j + 2 < n_kt) load_tile(j + 2, kl, vl);
+    load_tile(min(j + 2, n_kt - 1), kl, vl);   // unconditional: same loads in flight on every path
 
     // S^T tiles (raw scores): [key subtile kt2][query tile qt]
     f32x16 s[2][QT];
@@ -261,7 +266,7 @@ void attn_fwd_kernel(ExtendArgs a) {
           for (int qt = 0; qt < QT; ++qt)
             o[t][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[kt2][j2][t], pop[qt][kt2][j2], o[t][qt], 0, 0, 0);
 
-    if (j + 1 < n_kt) store_tile(buf ^ 1, ks_, vs_);
+    if (j + 1 < n_kt) store_tile(buf ^ 1, j + 1, ks_, vs_);
     __syncthreads();
   };
   for (int j = 0; j < n_kt; j += 2) {
