@@ -115,8 +115,17 @@ ExtendPlan plan_extend(const std::vector<int32_t>& slots, const std::vector<int6
       work.push_back({keys, {static_cast<int32_t>(i), q0}});
     }
   }
-  std::stable_sort(work.begin(), work.end(),
-                   [](const auto& a, const auto& b) { return a.first > b.first; });
+  // Conversation-major order: longest conversation first, its heaviest tiles first. Workgroups that
+  // run at the same time on one XCD then mostly belong to one conversation and sweep the same
+  // prefix K/V, so it stays in that XCD's L2; the heaviest tiles still start first.
+  std::vector<int64_t> conv_keys(lens.size(), 0);
+  for (auto& w : work) conv_keys[w.second.conv] = std::max(conv_keys[w.second.conv], w.first);
+  std::stable_sort(work.begin(), work.end(), [&](const auto& a, const auto& b) {
+    const int64_t ka = conv_keys[a.second.conv], kb = conv_keys[b.second.conv];
+    if (ka != kb) return ka > kb;
+    if (a.second.conv != b.second.conv) return a.second.conv < b.second.conv;
+    return a.first > b.first;
+  });
   plan.tiles.reserve(work.size());
   for (auto& w : work) plan.tiles.push_back(w.second);
   return plan;

@@ -113,7 +113,7 @@ struct ExtendTile {
 struct ExtendPlan {
   int32_t q_tile = 64;
   std::vector<ExtendConvDesc> convs;
-  std::vector<ExtendTile> tiles;  // sorted by decreasing key count (longest first)
+  std::vector<ExtendTile> tiles;  // conversation-major (longest conversation first), heaviest tile first
 };
 
 ExtendPlan plan_extend(const std::vector<int32_t>& slots, const std::vector<int64_t>& lens,
