@@ -107,22 +107,26 @@ void attn_fwd_kernel(ExtendArgs a) {
       vreg[u] = ld16(blk + kPageTokens * D + w * 8);        // V^T: dim w/2, keys 8*(w%2)..+8
     }
   };
+  // LDS store of a staged tile. Only a tile that reaches past the end of the conversation needs
+  // masking (uniform branch): K rows of pages past the end are zeroed and V of keys past the end
+  // is zeroed, so no value read from a clamped page can reach the output.
   auto store_tile = [&](int buf, int j, const uint4 (&kreg)[PER], const uint4 (&vreg)[PER]) {
+    const bool tail = kBN * (j + 1) > cd.len;
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int i = tid + u * NT;
       const int p = i / (2 * D), w = i % (2 * D);
       const int row = kPageTokens * p + w / (D / 8), col8 = (w % (D / 8)) * 8;
-      const bool in_conv = 4 * j + p < n_pg;
-      st16(&sm.k[buf][row][col8], in_conv ? kreg[u] : make_uint4(0, 0, 0, 0));
-      uint4 vx = vreg[u];
-      const int key0 = kBN * j + kPageTokens * p + 8 * (w & 1);
-      if (key0 + 8 > cd.len) {                              // zero V of keys past the end
+      uint4 kx = kreg[u], vx = vreg[u];
+      if (tail) {
+        if (4 * j + p >= n_pg) kx = make_uint4(0, 0, 0, 0);
+        const int key0 = kBN * j + kPageTokens * p + 8 * (w & 1);
         vx.x = mask_bf16x2(vx.x, key0 + 0 < cd.len, key0 + 1 < cd.len);
         vx.y = mask_bf16x2(vx.y, key0 + 2 < cd.len, key0 + 3 < cd.len);
         vx.z = mask_bf16x2(vx.z, key0 + 4 < cd.len, key0 + 5 < cd.len);
         vx.w = mask_bf16x2(vx.w, key0 + 6 < cd.len, key0 + 7 < cd.len);
       }
+      st16(&sm.k[buf][row][col8], kx);
       const int dim = w >> 1, c0 = 2 * (w & 1);             // key groups c0, c0+1 of the page
       uint16_t* vrow = &sm.v[buf][dim][kPageTokens * p];
       st8(vrow + 4 * vt_group_pos(c0), make_uint2(vx.x, vx.y));
@@ -266,7 +270,9 @@ void attn_fwd_kernel(ExtendArgs a) {
           for (int qt = 0; qt < QT; ++qt)
             o[t][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[kt2][j2][t], pop[qt][kt2][j2], o[t][qt], 0, 0, 0);
 
-    if (j + 1 < n_kt) store_tile(buf ^ 1, j + 1, ks_, vs_);
+    // Unconditional: past the last tile it stores a masked tile that is never read (the buffer's
+    // previous tile was consumed before the last barrier), and the store needs no branch.
+    store_tile(buf ^ 1, j + 1, ks_, vs_);
     __syncthreads();
   };
   for (int j = 0; j < n_kt; j += 2) {
