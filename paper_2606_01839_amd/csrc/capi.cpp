@@ -48,7 +48,8 @@ WsLayout ws_layout(const cs_pool_desc& d) {
   w.page_table = 0;
   size_t pt_bytes = static_cast<size_t>(d.max_convs) * static_cast<size_t>(d.max_pages_per_conv) * 4;
   w.partials = align_up(pt_bytes, kAlign);
-  w.partial_floats = static_cast<size_t>(max_decode_items(d)) * d.n_kv_heads * group * (d.head_dim + 2);
+  w.partial_floats =
+      static_cast<size_t>(max_decode_items(d)) * d.n_kv_heads * group * cs::partial_floats(d.head_dim);
   w.ring = align_up(w.partials + w.partial_floats * 4, kAlign);
   w.total = w.ring + kRingBytes;
   return w;

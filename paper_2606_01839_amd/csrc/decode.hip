@@ -33,7 +33,7 @@ struct DecodeArgs {
   int split;  // keys per split, multiple of 32, <= 1024
   const uint16_t* q;
   uint16_t* out;
-  float* partials;  // [n_items * n_kv_heads][group][D + 2]
+  float* partials;  // [n_items * n_kv_heads][group] records of partial_floats(D)
   float scale_log2;
 };
 
@@ -158,7 +158,7 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   l_run += xor_shfl(l_run, 16);
   l_run += xor_shfl(l_run, 32);
   if (c < a.group) {
-    float* pp = a.partials + (static_cast<size_t>(work) * a.group + c) * (D + 2);
+    float* pp = a.partials + (static_cast<size_t>(work) * a.group + c) * partial_floats(D);
 #pragma unroll
     for (int t = 0; t < DT; ++t)
 #pragma unroll
@@ -170,34 +170,61 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   }
 }
 
-// One wave per (conversation, query head): log-sum-exp merge of its splits in split order.
+// One workgroup per (conversation, query head): log-sum-exp merge of its splits, in three steps
+// whose order depends only on the split count (bitwise deterministic): the maximum M of the split
+// maxima; per thread, the weighted sum over a fixed subset of the splits (split group sg = thread /
+// (D/4) takes splits sg, sg + SG, ...; dim group = 4 consecutive dims, one 16-byte load); then the
+// split groups added in order 0 .. SG-1.
 template <int D>
-__global__ __launch_bounds__(64) void decode_merge_kernel(DecodeArgs a) {
-  constexpr int PER = D / 64;
+__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
+  constexpr int DV = D / 4;          // dim groups (4 dims each)
+  constexpr int SG = 256 / DV;       // split groups
+  constexpr int R = partial_floats(D);
+  __shared__ float red_o[SG][D];
+  __shared__ float red_l[SG];
+  __shared__ float wave_max[4];
   const int b = blockIdx.x, h = blockIdx.y;
   const int g = h / a.group, c = h % a.group;
   const DecodeConvDesc cd = a.convs[b];
-  const int lane = threadIdx.x;
-  auto part = [&](int s) {
-    return a.partials +
-           ((static_cast<size_t>(cd.item_start + s) * a.n_kv_heads + g) * a.group + c) * (D + 2);
-  };
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const size_t split_stride = static_cast<size_t>(a.n_kv_heads) * a.group * R;
+  const float* base =
+      a.partials + ((static_cast<size_t>(cd.item_start) * a.n_kv_heads + g) * a.group + c) * R;
+  const int n = cd.n_splits;
+
   float M = -INFINITY;
-  for (int s = 0; s < cd.n_splits; ++s) M = fmaxf(M, part(s)[D]);
-  float den = 0.f, acc[PER];
+  for (int s = tid; s < n; s += 256) M = fmaxf(M, base[s * split_stride + D]);
 #pragma unroll
-  for (int i = 0; i < PER; ++i) acc[i] = 0.f;
-  for (int s = 0; s < cd.n_splits; ++s) {
-    const float* p = part(s);
-    const float w = fast_exp2(p[D] - M);
-    den += w * p[D + 1];
-#pragma unroll
-    for (int i = 0; i < PER; ++i) acc[i] += w * p[lane + 64 * i];
+  for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, xor_shfl(M, off));
+  if (lane == 0) wave_max[wave] = M;
+  __syncthreads();
+  M = fmaxf(fmaxf(wave_max[0], wave_max[1]), fmaxf(wave_max[2], wave_max[3]));
+
+  const int dg = tid % DV, sg = tid / DV;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float den = 0.f;
+#pragma unroll 4
+  for (int s = sg; s < n; s += SG) {
+    const float* p = base + s * split_stride;
+    const f32x2 ml = *reinterpret_cast<const f32x2*>(p + D);
+    const f32x4 v = *reinterpret_cast<const f32x4*>(p + 4 * dg);
+    const float w = fast_exp2(ml.x - M);
+    acc += w * v;
+    den += w * ml.y;
   }
-  const float inv = 1.f / den;
-  uint16_t* orow = a.out + (static_cast<size_t>(b) * a.n_kv_heads * a.group + h) * D;
+  *reinterpret_cast<f32x4*>(&red_o[sg][4 * dg]) = acc;
+  if (dg == 0) red_l[sg] = den;
+  __syncthreads();
+  if (tid < D) {
+    float o = 0.f, l = 0.f;
 #pragma unroll
-  for (int i = 0; i < PER; ++i) orow[lane + 64 * i] = static_cast<uint16_t>(pack_bf16x2(acc[i] * inv, 0.f) & 0xFFFFu);
+    for (int k = 0; k < SG; ++k) {
+      o += red_o[k][tid];
+      l += red_l[k];
+    }
+    uint16_t* orow = a.out + (static_cast<size_t>(b) * a.n_kv_heads * a.group + h) * D;
+    orow[tid] = static_cast<uint16_t>(pack_bf16x2(o / l, 0.f) & 0xFFFFu);
+  }
 }
 
 static DecodeArgs make_args(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs, int n_convs,
@@ -239,8 +266,8 @@ hipError_t launch_decode_merge(const PoolGeom& g, const DecodeConvDesc* d_convs,
   if (n_convs == 0) return hipSuccess;
   const DecodeArgs a = make_args(g, 0, d_convs, n_convs, 0, 0, nullptr, out, partials);
   const dim3 grid(n_convs, g.n_q_heads);
-  if (g.head_dim == 128) decode_merge_kernel<128><<<grid, 64, 0, stream>>>(a);
-  else if (g.head_dim == 64) decode_merge_kernel<64><<<grid, 64, 0, stream>>>(a);
+  if (g.head_dim == 128) decode_merge_kernel<128><<<grid, 256, 0, stream>>>(a);
+  else if (g.head_dim == 64) decode_merge_kernel<64><<<grid, 256, 0, stream>>>(a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

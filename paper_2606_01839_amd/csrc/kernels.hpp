@@ -30,6 +30,10 @@ hipError_t launch_pack(const PoolGeom& g, int slot, int64_t len, void* wire, hip
 hipError_t launch_unpack(const PoolGeom& g, const void* wire, const int32_t* d_pages, int slot,
                          int64_t len, int lp0, int n_lp, hipStream_t stream);
 
+// Decode partial record of one (work item, query head): o[d], running max m, sum l, two unused
+// floats, so records stay 16-byte aligned.
+constexpr int partial_floats(int head_dim) { return head_dim + 4; }
+
 // Decode: split kernel over plan items (partials), then the merge kernel (output).
 hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs,
                                int n_convs, int n_items, int split_tokens, const void* q,
