@@ -553,6 +553,12 @@ def bench_mixed(args):
         "completed": stats["completed"], "tokens_per_s": tot["tokens"] / tot["wall_s"] if tot["wall_s"] else None,
         "step_ms": 1e3 * tot["wall_s"] / max(1, tot["steps"]),
         "decode_tokens": tot["dec_tokens"], "extend_tokens": tot["ext_tokens"],
+        "step_decode_gbs": gbs(tot["dec_bytes"], 1e3 * tot["wall_s"]),
+        "step_extend_tflops": tfs(tot["ext_flops"], 1e3 * tot["wall_s"]),
+        "note": "step_* rates: the step's decode bytes / extend FLOPs over the whole step wall time "
+                "(the two run concurrently: extend launches on a second stream). Per-kernel rates "
+                "below use each kernel's own event-timed duration, which includes the time it "
+                "shares the GPU with the other stream.",
         "decode_gbs": gbs(tot["dec_bytes"], tot["split_ms"] + tot["merge_ms"]),
         "decode_split_gbs": gbs(tot["dec_bytes"], tot["split_ms"]),
         "extend_tflops": tfs(tot["ext_flops"], tot["fwd_ms"]),

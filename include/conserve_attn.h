@@ -175,7 +175,10 @@ cs_status cs_attn_decode_batch(cs_pool* pool, int32_t n_convs, const cs_conv* co
  *   k, v:     [n_layers][sum(ext_lens) + n_dec][n_kv_heads][head_dim], extend tokens first
  *   q_ext:    [n_layers][sum(ext_lens)][n_q_heads][head_dim];  out_ext same shape
  *   q_dec:    [n_layers][n_dec][n_q_heads][head_dim];          out_dec same shape
- * The batch metadata is uploaded once and reused by every layer's launches.
+ * The batch metadata is uploaded once and reused by every layer's launches. When both parts are
+ * present, the extend launches run on a second stream owned by the pool, forked from `stream`
+ * after the append and joined back into it before the call returns: work enqueued on `stream`
+ * afterwards (and a synchronisation of `stream`) sees every output of the step.
  * Errors: as cs_kv_append_batch, cs_attn_extend and cs_attn_decode_batch.
  */
 cs_status cs_mixed_step(cs_pool* pool, int32_t n_ext, const cs_conv* ext_convs,

@@ -96,6 +96,9 @@ struct cs_pool {
   hipEvent_t switch_ev = nullptr;
   hipStream_t stream = nullptr;
   bool have_stream = false;
+  // second stream of cs_mixed_step (extend chunks run on it concurrently with the decode batch)
+  hipStream_t side = nullptr;
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   // instrumentation: timing events around each kernel launch while enabled
   struct ProfEvent {
     hipEvent_t start, stop;
@@ -182,20 +185,44 @@ hipError_t take_event(cs_pool* p, hipEvent_t* e) {
   return hipEventCreate(e);
 }
 
-// Launch a kernel; while profiling, bracket it with timing events on the pool's stream.
+// Launch a kernel on stream `s`; while profiling, bracket it with timing events on that stream.
 template <typename F>
-cs_status timed_launch(cs_pool* p, int kind, const char* what, F&& launch) {
+cs_status timed_launch_on(cs_pool* p, hipStream_t s, int kind, const char* what, F&& launch) {
   hipEvent_t a = nullptr, b = nullptr;
   if (p->prof_on) {
     CS_HIP(take_event(p, &a), "hipEventCreate");
     CS_HIP(take_event(p, &b), "hipEventCreate");
-    CS_HIP(hipEventRecord(a, p->stream), "hipEventRecord");
+    CS_HIP(hipEventRecord(a, s), "hipEventRecord");
   }
   CS_HIP(launch(), what);
   if (p->prof_on) {
-    CS_HIP(hipEventRecord(b, p->stream), "hipEventRecord");
+    CS_HIP(hipEventRecord(b, s), "hipEventRecord");
     p->prof_events.push_back({a, b, kind});
   }
+  return CS_OK;
+}
+
+template <typename F>
+cs_status timed_launch(cs_pool* p, int kind, const char* what, F&& launch) {
+  return timed_launch_on(p, p->stream, kind, what, launch);
+}
+
+// The second stream and its fork/join events, created on first use.
+cs_status ensure_side(cs_pool* p) {
+  if (p->side) return CS_OK;
+  hipStream_t s = nullptr;
+  CS_HIP(hipStreamCreateWithFlags(&s, hipStreamNonBlocking), "hipStreamCreate");
+  hipEvent_t f = nullptr, j = nullptr;
+  hipError_t e = hipEventCreateWithFlags(&f, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&j, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    if (f) (void)hipEventDestroy(f);
+    (void)hipStreamDestroy(s);
+    return hip_fail(e, "hipEventCreate");
+  }
+  p->side = s;
+  p->fork_ev = f;
+  p->join_ev = j;
   return CS_OK;
 }
 
@@ -303,11 +330,12 @@ cs_status upload_extend(cs_pool* p, const std::vector<int32_t>& slots, const std
   return CS_OK;
 }
 
-cs_status launch_extend_layer(cs_pool* p, const ExtendWork& w, int layer, const void* q, void* out) {
+cs_status launch_extend_layer(cs_pool* p, const ExtendWork& w, int layer, const void* q, void* out,
+                              hipStream_t s) {
   const cs::PoolGeom g = p->geom();
   for (const auto& pw : w.parts) {
-    cs_status st = timed_launch(p, CS_PROF_ATTN_FWD, "attention launch", [&] {
-      return cs::launch_extend(g, layer, pw.convs, pw.tiles, pw.n_tiles, q, out, p->stream);
+    cs_status st = timed_launch_on(p, s, CS_PROF_ATTN_FWD, "attention launch", [&] {
+      return cs::launch_extend(g, layer, pw.convs, pw.tiles, pw.n_tiles, q, out, s);
     });
     if (st != CS_OK) return st;
   }
@@ -377,7 +405,7 @@ cs_status attend(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* q_l
   }
   ExtendWork w;
   if ((st = upload_extend(p, slots, lens, ql, &w)) != CS_OK) return st;
-  return launch_extend_layer(p, w, layer, q, out);
+  return launch_extend_layer(p, w, layer, q, out, p->stream);
 }
 
 cs_status append_impl(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t* n_new,
@@ -481,6 +509,13 @@ cs_status cs_pool_destroy(cs_pool* p) {
       (void)hipEventDestroy(pe.stop);
     }
     (void)hipEventDestroy(p->switch_ev);
+    if (p->side) {
+      if (hipStreamSynchronize(p->side) != hipSuccess)
+        st = fail(CS_EHIP, "hipStreamSynchronize failed while destroying the pool");
+      (void)hipEventDestroy(p->fork_ev);
+      (void)hipEventDestroy(p->join_ev);
+      (void)hipStreamDestroy(p->side);
+    }
     (void)hipHostFree(p->h_ring);
   }
   delete p;
@@ -676,21 +711,34 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
   if (n_ext > 0 && (st = upload_extend(p, e_slots, e_lens, e_q, &ew)) != CS_OK) return st;
   if (n_dec > 0 && (st = upload_decode(p, d_slots, d_lens, &dw)) != CS_OK) return st;
   const size_t row_bytes = static_cast<size_t>(p->desc.n_q_heads) * p->desc.head_dim * 2;
-  for (int32_t layer = 0; layer < p->desc.n_layers; ++layer) {
-    if (n_ext > 0) {
-      const size_t off = static_cast<size_t>(layer) * static_cast<size_t>(ext_rows) * row_bytes;
-      if ((st = launch_extend_layer(p, ew, layer, static_cast<const char*>(q_ext) + off,
-                                    static_cast<char*>(out_ext) + off)) != CS_OK)
-        return st;
-    }
-    if (n_dec > 0) {
-      const size_t off = static_cast<size_t>(layer) * static_cast<size_t>(n_dec) * row_bytes;
-      if ((st = launch_decode_layer(p, dw, layer, static_cast<const char*>(q_dec) + off,
-                                    static_cast<char*>(out_dec) + off)) != CS_OK)
-        return st;
-    }
+  // Extend chunks and decode tokens of the step are independent once their K/V is appended: with
+  // both present the extend launches (all layers) go to a second stream that forks after the
+  // uploads and joins before the call returns, so the matrix-core-bound extend work overlaps the
+  // HBM-bound decode work.
+  const bool fork = n_ext > 0 && n_dec > 0;
+  hipStream_t ext_stream = p->stream;
+  if (fork) {
+    if ((st = ensure_side(p)) != CS_OK) return st;
+    CS_HIP(hipEventRecord(p->fork_ev, p->stream), "hipEventRecord");
+    CS_HIP(hipStreamWaitEvent(p->side, p->fork_ev, 0), "hipStreamWaitEvent");
+    ext_stream = p->side;
   }
-  return CS_OK;
+  for (int32_t layer = 0; layer < p->desc.n_layers && n_ext > 0; ++layer) {
+    const size_t off = static_cast<size_t>(layer) * static_cast<size_t>(ext_rows) * row_bytes;
+    if ((st = launch_extend_layer(p, ew, layer, static_cast<const char*>(q_ext) + off,
+                                  static_cast<char*>(out_ext) + off, ext_stream)) != CS_OK)
+      break;
+  }
+  for (int32_t layer = 0; layer < p->desc.n_layers && n_dec > 0 && st == CS_OK; ++layer) {
+    const size_t off = static_cast<size_t>(layer) * static_cast<size_t>(n_dec) * row_bytes;
+    st = launch_decode_layer(p, dw, layer, static_cast<const char*>(q_dec) + off,
+                             static_cast<char*>(out_dec) + off);
+  }
+  if (fork) {  // join even after a failed launch, so later work never overtakes the side stream
+    CS_HIP(hipEventRecord(p->join_ev, p->side), "hipEventRecord");
+    CS_HIP(hipStreamWaitEvent(p->stream, p->join_ev, 0), "hipStreamWaitEvent");
+  }
+  return st;
 }
 
 cs_status cs_profile_start(cs_pool* p) {
