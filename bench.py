@@ -553,12 +553,15 @@ def bench_mixed(args):
         "completed": stats["completed"], "tokens_per_s": tot["tokens"] / tot["wall_s"] if tot["wall_s"] else None,
         "step_ms": 1e3 * tot["wall_s"] / max(1, tot["steps"]),
         "decode_tokens": tot["dec_tokens"], "extend_tokens": tot["ext_tokens"],
-        "step_decode_gbs": gbs(tot["dec_bytes"], 1e3 * tot["wall_s"]),
-        "step_extend_tflops": tfs(tot["ext_flops"], 1e3 * tot["wall_s"]),
-        "note": "step_* rates: the step's decode bytes / extend FLOPs over the whole step wall time "
-                "(the two run concurrently: extend launches on a second stream). Per-kernel rates "
-                "below use each kernel's own event-timed duration, which includes the time it "
-                "shares the GPU with the other stream.",
+        "step_roofline": {
+            "decode_bytes_per_step": tot["dec_bytes"] / max(1, tot["steps"]),
+            "extend_flops_per_step": tot["ext_flops"] / max(1, tot["steps"]),
+            "roofline_ms_per_step": 1e3 * (tot["dec_bytes"] / (HBM_PEAK_GBS * 1e9) + tot["ext_flops"] / (BF16_PEAK_TFLOPS * 1e12)) / max(1, tot["steps"]),
+            "frac": (tot["dec_bytes"] / (HBM_PEAK_GBS * 1e9) + tot["ext_flops"] / (BF16_PEAK_TFLOPS * 1e12)) / tot["wall_s"] if tot["wall_s"] else None,
+            "note": "time the step's decode bytes take at 8 TB/s plus its extend FLOPs at 2.5 PFLOP/s, "
+                    "over the measured step time (extend runs on a second stream, overlapping the "
+                    "decode). Per-kernel rates below use each kernel's own event-timed duration, "
+                    "which includes the time it shares the GPU with the other stream."},
         "decode_gbs": gbs(tot["dec_bytes"], tot["split_ms"] + tot["merge_ms"]),
         "decode_split_gbs": gbs(tot["dec_bytes"], tot["split_ms"]),
         "extend_tflops": tfs(tot["ext_flops"], tot["fwd_ms"]),
