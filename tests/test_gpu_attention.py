@@ -151,6 +151,42 @@ def test_chunked_extend_matches_one_shot_prefill():
     pool.close()
 
 
+def test_aligned_chunked_prefill_is_bitwise_one_shot():
+    """Chunked turn-1 prefill (the prefiller's chunked prefill, Section 5.1) with chunks that are
+    multiples of the 64-query tile: every query tile sweeps the same key tiles in the same order as
+    in the one-shot prefill, so the outputs agree bit for bit (and both match the oracle)."""
+    hq, hkv, d = 32, 8, 128
+    lens, chunk = [700, 300], 256
+    pool = _pool(hq, hkv, d, 2 * sum((L + 15) // 16 for L in lens) + 8)
+    one = [pool.conv_create() for _ in lens]
+    kv = [kv_tokens(SEED, b, 1, 0, L, hkv, d) for b, L in enumerate(lens)]
+    for c, (k, v) in zip(one, kv):
+        pool.kv_append(c, k.cuda(), v.cuda())
+    qs = [q_tokens(SEED, b, 0, 0, L, hq, d).cuda() for b, L in enumerate(lens)]
+    full = pool.attn_prefill_turn1(one, lens, 0, torch.cat(qs))
+    ch = [pool.conv_create() for _ in lens]
+    got = [[] for _ in lens]
+    for s0 in range(0, max(lens), chunk):
+        act = [b for b, L in enumerate(lens) if L > s0]
+        n = [min(chunk, lens[b] - s0) for b in act]
+        k = torch.cat([kv[b][0][:, s0:s0 + nb] for b, nb in zip(act, n)], dim=1).contiguous().cuda()
+        v = torch.cat([kv[b][1][:, s0:s0 + nb] for b, nb in zip(act, n)], dim=1).contiguous().cuda()
+        pool.kv_append_batch([ch[b] for b in act], n, k, v)
+        out = pool.attn_extend([ch[b] for b in act], n, 0,
+                               torch.cat([qs[b][s0:s0 + nb] for b, nb in zip(act, n)]))
+        r = 0
+        for b, nb in zip(act, n):
+            got[b].append(out[r:r + nb])
+            r += nb
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat([torch.cat(g) for g in got]), full)
+    for b, L in enumerate(lens):
+        k, v = kv[b]
+        row0 = sum(lens[:b])
+        assert_close(full[row0:row0 + L], attend_last(f64(qs[b]), f64(k[0]), f64(v[0])), f"conv {b}")
+    pool.close()
+
+
 def test_nan_poisoned_pool_does_not_leak():
     """Every page starts as NaN; appends zero their pages' tails, so nothing past a conversation's
     end (or in never-used pages) can reach the outputs."""
