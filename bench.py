@@ -80,6 +80,37 @@ def traffic_per_launch(workload: str):
     return t.get("traffic_bytes_per_launch")
 
 
+def energy_run(fn, seconds=8.0):
+    """Run fn back to back for about `seconds` and read the GPU's energy accumulator (amdsmi)
+    before and after: joules, the firmware's own time base, average watts and the call count.
+    None where the counter is unavailable. Power is sampled, not controlled."""
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+        h = amdsmi.amdsmi_get_processor_handles()[0]
+        read = lambda: amdsmi.amdsmi_get_energy_count(h)
+        read()
+    except Exception:
+        return None
+    fn()
+    torch.cuda.synchronize()
+    e0 = read()
+    t0 = time.perf_counter()
+    n = 0
+    while time.perf_counter() - t0 < seconds:
+        fn()
+        n += 1
+        if n % 4 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    e1 = read()
+    joules = (e1["energy_accumulator"] - e0["energy_accumulator"]) * e1["counter_resolution"] * 1e-6
+    fw_s = (e1["timestamp"] - e0["timestamp"]) * 1e-9
+    watts = joules / fw_s if fw_s > 0 else None
+    return {"calls": n, "wall_s": wall, "joules": joules, "counter_s": fw_s, "avg_watts": watts}
+
+
 def timed(fn, steps, warmup):
     for _ in range(warmup):
         fn()
@@ -199,6 +230,7 @@ def bench_decode(args):
     step = lambda: pool.attn_decode_batch(convs, 0, q, out)
     ms = timed(step, args.steps, args.warmup)
     prof = profiled(pool, step, args.steps)
+    en = energy_run(step) if args.energy else None
     split_ms = prof["decode_split"][0] / max(1, prof["decode_split"][1])
     merge_ms = prof["decode_merge"][0] / max(1, prof["decode_merge"][1])
 
@@ -218,10 +250,10 @@ def bench_decode(args):
         L = int(lens[b])
         kh, vh = gen_kv(tr.seed, b, 0, min(L, 4096), hkv, d, sk, svs, device="cpu")
         assert torch.equal(kh, kv_dev[b][0][:min(L, 4096)].cpu()) and torch.equal(vh, kv_dev[b][1][:min(L, 4096)].cpu())
+    host = [(sv.bf16_to_f64(kv_dev[b][0]), sv.bf16_to_f64(kv_dev[b][1]), sv.bf16_to_f64(q[b:b + 1]))
+            for b in range(len(lens))]
     for b, L in enumerate(lens):
-        kf = sv.bf16_to_f64(kv_dev[b][0])
-        vf = sv.bf16_to_f64(kv_dev[b][1])
-        qf = sv.bf16_to_f64(q[b:b + 1])
+        kf, vf, qf = host[b]
         t = time.perf_counter()
         ref = attend_rows(qf, [int(L) - 1], kf, vf)
         cpu_s += time.perf_counter() - t
@@ -230,6 +262,16 @@ def bench_decode(args):
         num += float((diff ** 2).sum())
         den += float((ref ** 2).sum())
     rel_l2 = math.sqrt(num / den)
+    # the oracle's timing: whole decode steps repeated until about 10 s of CPU work
+    passes = 1
+    while cpu_s < 10.0 and passes < 16:
+        t = time.perf_counter()
+        for b, L in enumerate(lens):
+            kf, vf, qf = host[b]
+            attend_rows(qf, [int(L) - 1], kf, vf)
+        cpu_s += time.perf_counter() - t
+        passes += 1
+    del host
     workload = (f"decode batch: {len(lens)} conversations, context U[{tr.lo},{tr.hi}] (sum "
                 f"{int(lens.sum())} tokens), {hq}q/{hkv}kv heads, head_dim {d}, bf16 K/V x per-head "
                 f"scale U[{tr.scale_lo},{tr.scale_hi}], 16-token pages randomly placed, 1 layer")
@@ -243,12 +285,16 @@ def bench_decode(args):
         "step_bytes": step_bytes,
         "workload": workload,
         "traffic": traffic,
+        "energy": None if not en or not en["avg_watts"] else {
+            **en, "tokens_per_joule": en["calls"] * len(lens) / en["wall_s"] / en["avg_watts"],
+            "gb_per_joule": en["calls"] * step_bytes / 1e9 / en["wall_s"] / en["avg_watts"]},
         "parity": {"convs": len(lens), "max_abs": max_abs, "rel_l2": rel_l2,
                    "ok": bool(max_abs <= 1e-2 and rel_l2 <= 3e-3)},
-        "cpu": {"value": step_bytes / cpu_s / 1e9, "unit": "GB/s", "cores": blas_threads(),
+        "cpu": {"value": passes * step_bytes / cpu_s / 1e9, "unit": "GB/s", "cores": blas_threads(),
                 "kind": "oracle",
                 "sample": f"fp64 oracle over all {len(lens)} conversations x {hq} heads of the same "
-                          f"decode step (inputs already in host memory as fp64); {cpu_s:.2f} s"},
+                          f"decode step (inputs already in host memory as fp64), {passes} passes "
+                          f"in {cpu_s:.1f} s"},
     }
     pool.close()
     del kv_dev
@@ -383,6 +429,7 @@ def bench_prefill_transfer(args):
     prof = profiled(pre, step, reps)
     fwd_ms = prof["attn_fwd"][0] / max(1, prof["attn_fwd"][1])
     flops = attn_flops([0] * len(lens), lens, hq, d)
+    en = energy_run(step) if args.energy else None
     chunked = chunked_prefill(tr, lens, q, out, mk)
     # one-time transfer: pack every conversation, unpack into a pool with other placement
     dst = mk(tr.dst_seed)
@@ -412,6 +459,9 @@ def bench_prefill_transfer(args):
                     "roofline": {"bound": "mfma", "achieved": flops / (fwd_ms * 1e-3) / 1e12,
                                  "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                                  "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS}},
+        "prefill_energy": None if not en or not en["avg_watts"] else {
+            **en, "tokens_per_joule": en["calls"] * int(lens.sum()) / en["wall_s"] / en["avg_watts"],
+            "tflop_per_joule": en["calls"] * flops / 1e12 / en["wall_s"] / en["avg_watts"]},
         "prefill_chunked": chunked,
         "pack": {"kernel_ms": pk[0], "launches": pk[1], "bytes": move, "gbs": gbs(move, pk[0]),
                  "roofline": {"bound": "hbm", "achieved": gbs(move, pk[0]), "peak": HBM_PEAK_GBS,
@@ -648,6 +698,8 @@ def main():
                     help="run one component and print only its JSON (for profiling)")
     ap.add_argument("--mixed-steps", type=int, default=300,
                     help="timed steps of the mixed agentic trace component (0 = skip it)")
+    ap.add_argument("--no-energy", dest="energy", action="store_false",
+                    help="skip the energy runs (8 s of decode and 8 s of prefill, amdsmi counter)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB copy (for counter calibration under rocprofv3)")
     args = ap.parse_args()
@@ -695,6 +747,7 @@ def main():
                      "kernel_ms": round(dec["split_ms"], 4), "merge_kernel_ms": round(dec["merge_ms"], 4)},
         "cpu_baseline": dec["cpu"],
         "parity": dec["parity"],
+        "energy": dec["energy"],
         "components": comps,
     }
     print(json.dumps(line), flush=True)
