@@ -1,18 +1,22 @@
 // Turn-1 prefill and turn-N extend-prefill attention over paged KV (flash-attention forward).
 //
 // A workgroup owns one (conversation, 64-query block, kv head) tile; its waves cover the G query
-// heads of that kv head (the GQA group) -- at head_dim 128 two waves per head, 32 queries each,
-// two waves per SIMD -- so every K/V tile staged in LDS serves 64*G query rows.
+// heads of that kv head (the GQA group), so every K/V tile in LDS serves 64*G query rows.
 // Each wave computes the transposed score tile on the matrix cores (v_mfma_f32_32x32x16_bf16):
 //   S^T[key][query] = K[key][:] . Q[query][:]       A = K rows from LDS, B = Q kept in registers
 //   O^T[dim][query] += V^T[dim][key] . P^T[key][query]   A = V^T rows from LDS, B = P registers
-// With the transposed formulation every lane owns one query row (32 rows of a 32x32 tile, the
-// two 32-lane halves holding alternating groups of 4 keys), so the online-softmax max/sum are
-// in-lane except for one exchange between the halves, and the P accumulator registers are
-// directly the B operand of the PV product (the key order inside V^T is permuted in LDS to match).
-// K/V tiles of 64 keys (4 pages) are double-buffered in LDS and their global loads are issued two
-// tiles ahead (page ids through scalar loads, no branches around the loads, so the compiler's
-// vector-memory waits only ever wait for the older tile); fully visible tiles skip the mask.
+// With the transposed formulation every lane owns one query row (32 rows of a 32x32 tile, the two
+// 32-lane halves holding different keys), so the online-softmax max/sum are in-lane except for
+// one exchange between the halves, and the P accumulator registers are directly the B operand of
+// the PV product: the key order of K or V^T in LDS is arranged so the two contractions agree.
+//
+// head_dim 128 (attn_fwd_kernel): two waves per query head (32 queries each), two waves per SIMD.
+// K/V tiles of 64 keys (4 pages) are copied from HBM straight into a four-deep LDS ring with
+// global_load_lds_dwordx4 (no staging registers, no LDS store instructions), three tiles ahead;
+// the K operands of tile j+1 are read into registers while the PV product of tile j runs.
+// head_dim 64 (attn_fwd_staged_kernel): one wave per query head (64 queries in two 32-row tiles),
+// one wave per SIMD; K/V tiles staged through registers into a double-buffered LDS tile two tiles
+// ahead. In both, diagonal tiles apply the causal mask and fully visible tiles skip it.
 #include <cmath>
 
 #include "device_common.hpp"
@@ -37,6 +41,7 @@ struct ExtendArgs {
 constexpr int kBN = 64;  // keys per tile
 constexpr int kBM = 64;  // query tokens per workgroup
 
+// LDS tile of the staged kernel (padded rows: bank-conflict-free MFMA operand reads).
 template <int D>
 struct FwdSmem {
   static constexpr int kRowK = D + 8;    // K tile row stride (elements), padded
@@ -54,9 +59,256 @@ __device__ __forceinline__ int vt_group_pos(int c) { return ((c & 1) << 1) | (c 
 // a new score exceeds it by more than this, so P <= 2^8 and the O/l rescale is rare.
 constexpr float kRescaleLog2 = 8.f;
 
+// ------------------------------------------------------------------------------------------------
+// head_dim 128: K/V copied from HBM straight into LDS.
+// LDS layout of one ring buffer (32 KiB): K as 64 rows x 256 B, the 16-byte chunk index XOR-swizzled
+// by the row (chunk ^ (row & 15)); V^T page by page, 128 dims x 32 B (16 keys) per page, the two
+// 16-byte halves of a dim swapped when bit 2 of the dim is set. Both make the MFMA operand reads
+// bank-conflict free while every copy instruction still writes 1 KiB of consecutive LDS bytes.
+// ------------------------------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)p));
+}
+// Copy 16 bytes per lane from global memory (wave-uniform base + per-lane byte offset) straight
+// into LDS: lane l writes LDS bytes lds + 16 l .. +15 (global_load_lds_dwordx4, destination base in
+// M0). The copy is tracked by the vector-memory counter only; M0 is saved and restored around it.
+__device__ __forceinline__ void dma16(uint32_t lds, const void* gbase, uint32_t voff) {
+  uint32_t saved;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %2, %3\n\ts_mov_b32 m0, %0"
+               : "=&s"(saved) : "s"(lds), "v"(voff), "s"(gbase) : "memory");
+}
+// Wait until at most N of this wave's vector-memory operations (its copies) are in flight, then a
+// workgroup barrier: afterwards every wave's copies issued before its own last N have landed.
+template <int N>
+__device__ __forceinline__ void dma_wait_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" :: "n"(N) : "memory");
+}
+
+template <int G>
+__global__ __launch_bounds__(64 * G * (kBM / 32)) __attribute__((amdgpu_waves_per_eu(G >= 4 ? 2 : 1)))
+void attn_fwd_kernel(ExtendArgs a) {
+  constexpr int D = 128;
+  constexpr int NW = G * (kBM / 32);
+  constexpr int KS = D / 16;
+  constexpr int DT = D / 32;
+  constexpr int NB = 16;                  // 1 KiB blocks per K (and per V^T) tile
+  constexpr int BPW = NB / NW;            // blocks per wave
+  static_assert(NB % NW == 0 && BPW <= 4, "a wave's blocks must lie in one page");
+  constexpr int TILE = 32768;             // K + V^T bytes per buffer
+  constexpr int NBUF = 4;                 // LDS ring: tile j read, j+1 landed, j+2 and j+3 in flight
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NBUF * TILE];
+
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int tile_idx = blockIdx.x / a.n_kv_heads, g = blockIdx.x % a.n_kv_heads;
+  const ExtendTile tile = a.tiles[tile_idx];
+  const ExtendConvDesc cd = a.convs[tile.conv];
+  const int prefix = cd.len - cd.q_len;
+  const int q_hi = min(cd.q_len, tile.q0 + kBM);
+  const int pos_min = prefix + tile.q0, pos_max = prefix + q_hi - 1;
+  const int n_kt = pos_max / kBN + 1;
+  const int n_pg = (cd.len + kPageTokens - 1) / kPageTokens;
+  const int32_t* pt = a.page_table + static_cast<size_t>(cd.slot) * a.max_pages;
+  const int h = g * G + wave % G;
+  const int qblk = wave / G;
+  const int n_q_heads = a.n_kv_heads * G;
+  const size_t head_stride = static_cast<size_t>(2 * kPageTokens * D);
+  const size_t layer_base = static_cast<size_t>(a.layer) * a.n_pages * a.n_kv_heads * head_stride +
+                            static_cast<size_t>(g) * head_stride;
+  const size_t page_stride = static_cast<size_t>(a.n_kv_heads) * head_stride;
+  const float c = a.scale_log2;
+  const __attribute__((address_space(4))) int32_t* ptc =
+      (const __attribute__((address_space(4))) int32_t*)reinterpret_cast<uintptr_t>(pt);
+
+  // ---- copy side: block kb (1 KiB) of a tile = K rows 4kb .. 4kb+3 (page kb / 4) and V^T dims
+  // 32 (kb % 4) .. +31 of page kb / 4; this wave copies blocks BPW*wave .. BPW*wave + BPW-1, all of
+  // one page. The per-lane global offsets are fixed; only the page base changes per tile.
+  const int q_w = (BPW * wave) / 4;
+  uint32_t koff[BPW], voff[BPW];
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    const int quarter = (BPW * wave + i) % 4;
+    const int row = 4 * quarter + lane / 16;                 // LDS row within the page
+    const int chunk = (lane % 16) ^ row;                     // logical 16-byte chunk of that row
+    // LDS row 8a + 4h + b holds key 8h + 4a + b (bits 2 and 3 swapped): the S^T accumulator
+    // of lane half h then holds keys 8h .. 8h+7 of each 16-key step, the order of V^T in LDS.
+    const int key = ((quarter & 1) << 3 | (quarter >> 1) << 2) + lane / 16;
+    koff[i] = static_cast<uint32_t>(key * (2 * D) + chunk * 16);
+    const int dim = 32 * quarter + lane / 2;
+    const int hv = (lane & 1) ^ ((dim >> 2) & 1);
+    voff[i] = static_cast<uint32_t>(2 * kPageTokens * D + dim * 32 + hv * 16);
+  }
+  const uint32_t smem_base = lds_u32(smem);
+  auto copy_tile = [&](int j, int buf) {
+    const int lp = min(4 * j + q_w, n_pg - 1);
+    const uint16_t* blk = a.pool + layer_base + static_cast<size_t>(ptc[lp]) * page_stride;
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      const int kb = BPW * wave + i;
+      dma16(smem_base + buf * TILE + kb * 1024, blk, koff[i]);
+      dma16(smem_base + buf * TILE + 16384 + kb * 1024, blk, voff[i]);
+    }
+  };
+
+  // ---- read side: MFMA operand addresses (bytes within a buffer) -------------------------------
+  // K operand of lane (col, half) for k-step ks: LDS row col (+32 kt2), logical chunk 2 ks + half,
+  // stored at chunk (2 ks + half) ^ (row & 15). V^T operand for (kt2, j2, t): page 2 kt2 + j2,
+  // dims 32 t + col, keys 8 half .. +7, stored in the block 4 (2 kt2 + j2) + t at col * 32 +
+  // 16 (half ^ bit 2 of col).
+  const int half = lane >> 5, col = lane & 31;
+  uint32_t kaddr[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+    kaddr[ks] = static_cast<uint32_t>(col * (2 * D) + (((2 * ks + half) ^ (col & 15)) * 16));
+  const uint32_t vaddr = static_cast<uint32_t>(16384 + col * 32 + ((half ^ ((col >> 2) & 1)) * 16));
+
+  bf16x8 qop[KS];
+  int qpos;
+  {
+    const int qi = tile.q0 + 32 * qblk + col;
+    const bool valid = qi < cd.q_len;
+    qpos = prefix + (valid ? qi : cd.q_len - 1);
+    const uint16_t* qrow = a.q + (static_cast<size_t>(cd.q_row + (valid ? qi : 0)) * n_q_heads + h) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qop[ks] = valid ? as_bf16x8(ld16(qrow + 16 * ks + 8 * half)) : bf16x8{};
+  }
+  f32x16 o[DT];
+#pragma unroll
+  for (int t = 0; t < DT; ++t)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[t][e] = 0.f;
+  float m_s = -INFINITY, l_run = 0.f;
+  const bf16x2 ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+
+  // Copies are issued for tiles past the end too (clamped to the last tile, whose pages past the
+  // conversation's end are clamped to its last page), so every step issues the same number and
+  // the counter waits below stay exact. Those keys are masked by the causal mask.
+  copy_tile(0, 0);
+  copy_tile(min(1, n_kt - 1), 1);
+  copy_tile(min(2, n_kt - 1), 2);
+  dma_wait_barrier<2 * BPW>();   // tiles 0 and 1 landed
+  // K operands of the next tile are read into registers during the current tile's PV product.
+  bf16x8 kop[KS][2];
+  auto read_k = [&](int buf) {
+    const uint8_t* kb = smem + buf * TILE;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int kt2 = 0; kt2 < 2; ++kt2)
+        kop[ks][kt2] = as_bf16x8(ld16(kb + kaddr[ks] + kt2 * 8192));
+  };
+  read_k(0);
+
+  auto tile_step = [&](const int j, const int buf) {
+    copy_tile(min(j + 3, n_kt - 1), (buf + 3) % NBUF);
+    const uint8_t* kb = smem + buf * TILE;
+    f32x16 s[2];
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[kt2][e] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int kt2 = 0; kt2 < 2; ++kt2)
+        s[kt2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ks][kt2], qop[ks], s[kt2], 0, 0, 0);
+
+    bf16x8 vop[2][2][DT];
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+      for (int j2 = 0; j2 < 2; ++j2)
+#pragma unroll
+        for (int t = 0; t < DT; ++t)
+          vop[kt2][j2][t] = as_bf16x8(ld16(kb + vaddr + (4 * (2 * kt2 + j2) + t) * 1024));
+
+    if (kBN * j + kBN - 1 > pos_min) {
+#pragma unroll
+      for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = kBN * j + 32 * kt2 + 16 * (e >> 3) + 8 * half + 4 * ((e >> 2) & 1) + (e & 3);
+          if (key > qpos) s[kt2][e] = -INFINITY;
+        }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt2][e]);
+    mx = halves_max(mx) * c;
+    if (__builtin_amdgcn_ballot_w64(mx > m_s + kRescaleLog2) != 0) {
+      const float m_new = fmaxf(m_s, mx);
+      const float alpha = fast_exp2(m_s - m_new);
+      m_s = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < DT; ++t) o[t] *= alpha;
+    }
+    const float neg_m = -m_s;
+    float ps0 = 0.f, ps1 = 0.f;
+    bf16x8 pop[2][2];
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2) {
+      float p[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) p[e] = fast_exp2(__builtin_fmaf(s[kt2][e], c, neg_m));
+#pragma unroll
+      for (int j2 = 0; j2 < 2; ++j2) {
+        uint32_t w0 = pack_bf16x2(p[8 * j2 + 0], p[8 * j2 + 1]);
+        uint32_t w1 = pack_bf16x2(p[8 * j2 + 2], p[8 * j2 + 3]);
+        uint32_t w2 = pack_bf16x2(p[8 * j2 + 4], p[8 * j2 + 5]);
+        uint32_t w3 = pack_bf16x2(p[8 * j2 + 6], p[8 * j2 + 7]);
+        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), ones, ps0, false);
+        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), ones, ps1, false);
+        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w2), ones, ps0, false);
+        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w3), ones, ps1, false);
+        pop[kt2][j2] = __builtin_bit_cast(bf16x8, make_uint4(w0, w1, w2, w3));
+      }
+    }
+    l_run += ps0 + ps1;
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+      for (int j2 = 0; j2 < 2; ++j2)
+#pragma unroll
+        for (int t = 0; t < DT; ++t)
+          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[kt2][j2][t], pop[kt2][j2], o[t], 0, 0, 0);
+    read_k((buf + 1) % NBUF);      // tile j+1 is in LDS (waited at the end of step j-1)
+    // this wave's copies of tile j+2 have landed (those of tile j+3 may still fly); after the
+    // barrier every wave's have.
+    dma_wait_barrier<2 * BPW>();
+  };
+  for (int j = 0; j < n_kt; j += 4) {
+    tile_step(j, 0);
+    if (j + 1 < n_kt) tile_step(j + 1, 1);
+    if (j + 2 < n_kt) tile_step(j + 2, 2);
+    if (j + 3 < n_kt) tile_step(j + 3, 3);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no copy may land after the workgroup ends
+
+  const int qi = tile.q0 + 32 * qblk + col;
+  const float l_tot = halves_sum(l_run);
+  if (qi < cd.q_len) {
+    const float inv = 1.f / l_tot;
+    uint16_t* orow = a.out + (static_cast<size_t>(cd.q_row + qi) * n_q_heads + h) * D;
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int dim = 32 * t + 8 * e4 + 4 * half;
+        st8(orow + dim, make_uint2(pack_bf16x2(o[t][4 * e4 + 0] * inv, o[t][4 * e4 + 1] * inv),
+                                   pack_bf16x2(o[t][4 * e4 + 2] * inv, o[t][4 * e4 + 3] * inv)));
+      }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// head_dim 64: K/V staged through registers (global loads two tiles ahead, LDS stores of the next
+// tile at the end of a step); V^T 4-key groups permuted in LDS to the accumulator's key order.
+// ------------------------------------------------------------------------------------------------
 template <int D, int G, int QT, int BM>
 __global__ __launch_bounds__(64 * G * (BM / (32 * QT))) __attribute__((amdgpu_waves_per_eu(QT == 1 ? 2 : 1)))
-void attn_fwd_kernel(ExtendArgs a) {
+void attn_fwd_staged_kernel(ExtendArgs a) {
   constexpr int NW = G * (BM / (32 * QT));  // waves: G query heads x BM/(32 QT) query blocks
   constexpr int NT = 64 * NW;          // threads
   constexpr int KS = D / 16;           // k-steps of QK^T (16 dims each)
@@ -303,8 +555,11 @@ void attn_fwd_kernel(ExtendArgs a) {
 // per wave, G waves.
 template <int D, int G>
 static void launch_fwd(const ExtendArgs& a, int n_tiles, int n_kv_heads, hipStream_t stream) {
-  constexpr int QT = D == 64 ? 2 : 1;
-  attn_fwd_kernel<D, G, QT, kBM><<<n_tiles * n_kv_heads, 64 * G * (kBM / (32 * QT)), 0, stream>>>(a);
+  if constexpr (D == 128) {
+    attn_fwd_kernel<G><<<n_tiles * n_kv_heads, 64 * G * (kBM / 32), 0, stream>>>(a);
+  } else {
+    attn_fwd_staged_kernel<D, G, 2, kBM><<<n_tiles * n_kv_heads, 64 * G * (kBM / 64), 0, stream>>>(a);
+  }
 }
 
 int extend_query_tile(int) { return kBM; }
