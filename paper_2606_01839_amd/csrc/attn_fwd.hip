@@ -58,6 +58,8 @@ __device__ __forceinline__ int vt_group_pos(int c) { return ((c & 1) << 1) | (c 
 // Lazy rescaling threshold (log2 units): the running max used in the exponent is only raised when
 // a new score exceeds it by more than this, so P <= 2^8 and the O/l rescale is rare.
 constexpr float kRescaleLog2 = 8.f;
+// Per-lane bound on the sum of a tile's weights (32 keys per lane) before the max is refreshed.
+constexpr float kSumLimit = 256.f;
 
 // ------------------------------------------------------------------------------------------------
 // head_dim 128: K/V copied from HBM straight into LDS.
@@ -230,42 +232,50 @@ void attn_fwd_kernel(ExtendArgs a) {
           if (key > qpos) s[kt2][e] = -INFINITY;
         }
     }
-    float mx = -INFINITY;
+    // Weights against the running max m. If a lane's partial sum over its 32 keys of the tile
+    // exceeds 2^8 or is not finite (always on the first tile, where m = -inf), the wave takes the
+    // tile's row max, rescales O and l and recomputes the weights: every weight stays <= 2^8
+    // without a max reduction on the common path.
+    bf16x8 pop[2][2];
+    auto weights = [&](float neg_m) {
+      float ps0 = 0.f, ps1 = 0.f;
 #pragma unroll
-    for (int kt2 = 0; kt2 < 2; ++kt2)
+      for (int kt2 = 0; kt2 < 2; ++kt2) {
+        float p[16];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt2][e]);
-    mx = halves_max(mx) * c;
-    if (__builtin_amdgcn_ballot_w64(mx > m_s + kRescaleLog2) != 0) {
-      const float m_new = fmaxf(m_s, mx);
+        for (int e = 0; e < 16; ++e) p[e] = fast_exp2(__builtin_fmaf(s[kt2][e], c, neg_m));
+#pragma unroll
+        for (int j2 = 0; j2 < 2; ++j2) {
+          const uint4 pw = make_uint4(pack_bf16x2(p[8 * j2 + 0], p[8 * j2 + 1]),
+                                      pack_bf16x2(p[8 * j2 + 2], p[8 * j2 + 3]),
+                                      pack_bf16x2(p[8 * j2 + 4], p[8 * j2 + 5]),
+                                      pack_bf16x2(p[8 * j2 + 6], p[8 * j2 + 7]));
+          // the denominator sums the same bf16-rounded weights the PV product uses
+          ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw.x), ones, ps0, false);
+          ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw.y), ones, ps1, false);
+          ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw.z), ones, ps0, false);
+          ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw.w), ones, ps1, false);
+          pop[kt2][j2] = __builtin_bit_cast(bf16x8, pw);
+        }
+      }
+      return ps0 + ps1;
+    };
+    float ps = weights(-m_s);
+    if (__builtin_amdgcn_ballot_w64(!(ps <= kSumLimit)) != 0) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt2][e]);
+      const float m_new = fmaxf(m_s, halves_max(mx) * c);
       const float alpha = fast_exp2(m_s - m_new);
       m_s = m_new;
       l_run *= alpha;
 #pragma unroll
       for (int t = 0; t < DT; ++t) o[t] *= alpha;
+      ps = weights(-m_new);
     }
-    const float neg_m = -m_s;
-    float ps0 = 0.f, ps1 = 0.f;
-    bf16x8 pop[2][2];
-#pragma unroll
-    for (int kt2 = 0; kt2 < 2; ++kt2) {
-      float p[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e) p[e] = fast_exp2(__builtin_fmaf(s[kt2][e], c, neg_m));
-#pragma unroll
-      for (int j2 = 0; j2 < 2; ++j2) {
-        uint32_t w0 = pack_bf16x2(p[8 * j2 + 0], p[8 * j2 + 1]);
-        uint32_t w1 = pack_bf16x2(p[8 * j2 + 2], p[8 * j2 + 3]);
-        uint32_t w2 = pack_bf16x2(p[8 * j2 + 4], p[8 * j2 + 5]);
-        uint32_t w3 = pack_bf16x2(p[8 * j2 + 6], p[8 * j2 + 7]);
-        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), ones, ps0, false);
-        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), ones, ps1, false);
-        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w2), ones, ps0, false);
-        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w3), ones, ps1, false);
-        pop[kt2][j2] = __builtin_bit_cast(bf16x8, make_uint4(w0, w1, w2, w3));
-      }
-    }
-    l_run += ps0 + ps1;
+    l_run += ps;
 #pragma unroll
     for (int kt2 = 0; kt2 < 2; ++kt2)
 #pragma unroll
