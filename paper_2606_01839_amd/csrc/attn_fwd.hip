@@ -65,8 +65,10 @@ constexpr float kSumLimit = 256.f;
 // head_dim 128: K/V copied from HBM straight into LDS.
 // LDS layout of one ring buffer (32 KiB): K as 64 rows x 256 B, the 16-byte chunk index XOR-swizzled
 // by the row (chunk ^ (row & 15)); V^T page by page, 128 dims x 32 B (16 keys) per page, the two
-// 16-byte halves of a dim swapped when bit 2 of the dim is set. Both make the MFMA operand reads
-// bank-conflict free while every copy instruction still writes 1 KiB of consecutive LDS bytes.
+// 16-byte halves of a dim swapped when bit 2 xor bit 3 of the dim is set. A 16-byte operand read
+// is served 16 lanes at a time over 256 bytes of banks: the 16 rows (K) or dims (V^T) such a group
+// reads then fall in 16 distinct 16-byte bank groups (rocprofv3 SQ_LDS_BANK_CONFLICT = 0), while
+// every copy instruction still writes 1 KiB of consecutive LDS bytes.
 // ------------------------------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t lds_u32(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)p));
@@ -136,7 +138,7 @@ void attn_fwd_kernel(ExtendArgs a) {
     const int key = ((quarter & 1) << 3 | (quarter >> 1) << 2) + lane / 16;
     koff[i] = static_cast<uint32_t>(key * (2 * D) + chunk * 16);
     const int dim = 32 * quarter + lane / 2;
-    const int hv = (lane & 1) ^ ((dim >> 2) & 1);
+    const int hv = (lane & 1) ^ ((dim >> 2) & 1) ^ ((dim >> 3) & 1);
     voff[i] = static_cast<uint32_t>(2 * kPageTokens * D + dim * 32 + hv * 16);
   }
   const uint32_t smem_base = lds_u32(smem);
@@ -155,13 +157,14 @@ void attn_fwd_kernel(ExtendArgs a) {
   // K operand of lane (col, half) for k-step ks: LDS row col (+32 kt2), logical chunk 2 ks + half,
   // stored at chunk (2 ks + half) ^ (row & 15). V^T operand for (kt2, j2, t): page 2 kt2 + j2,
   // dims 32 t + col, keys 8 half .. +7, stored in the block 4 (2 kt2 + j2) + t at col * 32 +
-  // 16 (half ^ bit 2 of col).
+  // 16 (half ^ bit 2 of col ^ bit 3 of col).
   const int half = lane >> 5, col = lane & 31;
   uint32_t kaddr[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
     kaddr[ks] = static_cast<uint32_t>(col * (2 * D) + (((2 * ks + half) ^ (col & 15)) * 16));
-  const uint32_t vaddr = static_cast<uint32_t>(16384 + col * 32 + ((half ^ ((col >> 2) & 1)) * 16));
+  const uint32_t vaddr =
+      static_cast<uint32_t>(16384 + col * 32 + ((half ^ ((col >> 2) & 1) ^ ((col >> 3) & 1)) * 16));
 
   bf16x8 qop[KS];
   int qpos;
