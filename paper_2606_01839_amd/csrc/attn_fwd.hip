@@ -174,7 +174,14 @@ void attn_fwd_kernel(ExtendArgs a) {
     qpos = prefix + (valid ? qi : cd.q_len - 1);
     const uint16_t* qrow = a.q + (static_cast<size_t>(cd.q_row + (valid ? qi : 0)) * n_q_heads + h) * D;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qop[ks] = valid ? as_bf16x8(ld16(qrow + 16 * ks + 8 * half)) : bf16x8{};
+    for (int ks = 0; ks < KS; ++ks) {
+      const uint4 x = ld16(qrow + 16 * ks + 8 * half);      // in bounds for padding rows too
+      qop[ks] = as_bf16x8(valid ? x : make_uint4(0, 0, 0, 0));
+    }
+    // Q must have arrived before the loop: the compiler's own vector-memory waits then never
+    // extend to the copies the loop keeps in flight (a wait at the loop head would drain them).
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) asm volatile("" ::"v"(qop[ks]));
   }
   f32x16 o[DT];
 #pragma unroll
