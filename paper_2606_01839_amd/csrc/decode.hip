@@ -37,7 +37,24 @@ struct DecodeArgs {
   float scale_log2;
 };
 
-__device__ __forceinline__ int find_conv(const DecodeConvDesc* convs, int n, int item) {
+// Kernel arguments read by every wave alike are loaded through the constant address space, so
+// they land in scalar registers and the loop control, page bases and addresses stay wave-uniform.
+template <typename T>
+__device__ __forceinline__ const __attribute__((address_space(4))) T* as_const(const T* p) {
+  return (const __attribute__((address_space(4))) T*)reinterpret_cast<uintptr_t>(p);
+}
+
+__device__ __forceinline__ DecodeConvDesc load_desc(const __attribute__((address_space(4))) DecodeConvDesc* p) {
+  DecodeConvDesc d;
+  d.slot = p->slot;
+  d.len = p->len;
+  d.item_start = p->item_start;
+  d.n_splits = p->n_splits;
+  return d;
+}
+
+__device__ __forceinline__ int find_conv(const __attribute__((address_space(4))) DecodeConvDesc* convs,
+                                         int n, int item) {
   int lo = 0, hi = n - 1;
   while (lo < hi) {  // largest b with item_start <= item
     int mid = (lo + hi + 1) >> 1;
@@ -50,12 +67,13 @@ template <int D>
 __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   constexpr int KS = D / 32;  // k-steps of the QK^T contraction
   constexpr int DT = D / 16;  // 16-dim tiles of the output
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int work = blockIdx.x * 4 + wave;  // = item * n_kv_heads + kv head
   if (work >= a.n_items * a.n_kv_heads) return;
   const int item = work / a.n_kv_heads, g = work % a.n_kv_heads;
-  const int conv_idx = find_conv(a.convs, a.n_convs, item);
-  const DecodeConvDesc cd = a.convs[conv_idx];
+  const auto* convs = as_const(a.convs);
+  const int conv_idx = find_conv(convs, a.n_convs, item);
+  const DecodeConvDesc cd = load_desc(convs + conv_idx);
   const int k_begin = (item - cd.item_start) * a.split;
   const int k_end = min(cd.len, k_begin + a.split);
   const int n_pg = (k_end - k_begin + kPageTokens - 1) / kPageTokens;
@@ -81,28 +99,37 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   for (int t = 0; t < DT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const size_t head_stride = static_cast<size_t>(2 * kPageTokens * D);
-  const size_t layer_base = static_cast<size_t>(a.layer) * a.n_pages * a.n_kv_heads * head_stride +
-                            static_cast<size_t>(g) * head_stride;
+  const uint16_t* layer_base = a.pool + static_cast<size_t>(a.layer) * a.n_pages * a.n_kv_heads * head_stride +
+                               static_cast<size_t>(g) * head_stride;
+  const size_t page_stride = static_cast<size_t>(a.n_kv_heads) * head_stride;
+  // Per-lane byte offsets inside a page block (the same for every page): K row c, dims 8 qd ..;
+  // V^T row c (of a 16-dim tile), keys 4 qd .. 4 qd + 3.
+  const uint32_t koff = static_cast<uint32_t>((c * D + 8 * qd) * 2);
+  const uint32_t voff = static_cast<uint32_t>((kPageTokens * D + c * kPageTokens + 4 * qd) * 2);
 
   for (int j = 0; j < n_pg; j += 2) {
     const bool has_b = j + 1 < n_pg;
     const int pa = __builtin_amdgcn_readlane(pid, j);
     const int pb = has_b ? __builtin_amdgcn_readlane(pid, j + 1) : pa;
-    const uint16_t* blk_a = a.pool + layer_base + static_cast<size_t>(pa) * a.n_kv_heads * head_stride;
-    const uint16_t* blk_b = a.pool + layer_base + static_cast<size_t>(pb) * a.n_kv_heads * head_stride;
+    const uint8_t* blk_a = reinterpret_cast<const uint8_t*>(layer_base + static_cast<size_t>(pa) * page_stride);
+    const uint8_t* blk_b = reinterpret_cast<const uint8_t*>(layer_base + static_cast<size_t>(pb) * page_stride);
 
     bf16x8 ka[KS], kb[KS];
     uint2 va[DT], vb[DT];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      ka[ks] = as_bf16x8(ld16(blk_a + c * D + 32 * ks + 8 * qd));
-      kb[ks] = has_b ? as_bf16x8(ld16(blk_b + c * D + 32 * ks + 8 * qd)) : bf16x8{};
-    }
+    for (int ks = 0; ks < KS; ++ks) ka[ks] = as_bf16x8(ld16_nt(blk_a + koff + 64 * ks));
 #pragma unroll
-    for (int t = 0; t < DT; ++t) {
-      va[t] = ld8(blk_a + kPageTokens * D + (16 * t + c) * kPageTokens + 4 * qd);
-      vb[t] = has_b ? ld8(blk_b + kPageTokens * D + (16 * t + c) * kPageTokens + 4 * qd)
-                    : make_uint2(0, 0);
+    for (int t = 0; t < DT; ++t) va[t] = ld8_nt(blk_a + voff + 16 * kPageTokens * 2 * t);
+    if (has_b) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kb[ks] = as_bf16x8(ld16_nt(blk_b + koff + 64 * ks));
+#pragma unroll
+      for (int t = 0; t < DT; ++t) vb[t] = ld8_nt(blk_b + voff + 16 * kPageTokens * 2 * t);
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kb[ks] = bf16x8{};
+#pragma unroll
+      for (int t = 0; t < DT; ++t) vb[t] = make_uint2(0, 0);
     }
 
     f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
@@ -185,7 +212,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
   __shared__ float wave_max[4];
   const int b = blockIdx.x, h = blockIdx.y;
   const int g = h / a.group, c = h % a.group;
-  const DecodeConvDesc cd = a.convs[b];
+  const DecodeConvDesc cd = load_desc(as_const(a.convs) + b);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t split_stride = static_cast<size_t>(a.n_kv_heads) * a.group * R;
   const float* base =

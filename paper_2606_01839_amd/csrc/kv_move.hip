@@ -101,11 +101,11 @@ __global__ __launch_bounds__(64) void kv_pack_kernel(const uint16_t* __restrict_
   const int valid = rem < kPageTokens ? static_cast<int>(rem) : kPageTokens;
   uint4 x[kPerLane];
 #pragma unroll
-  for (int j = 0; j < kPerLane; ++j) x[j] = ld16(src + 8 * (threadIdx.x + 64 * j));
+  for (int j = 0; j < kPerLane; ++j) x[j] = ld16_nt(src + 8 * (threadIdx.x + 64 * j));
 #pragma unroll
   for (int j = 0; j < kPerLane; ++j) {
     const int i = threadIdx.x + 64 * j;
-    st16(dst + 8 * i, valid < kPageTokens ? mask_tail<D>(x[j], i, valid) : x[j]);
+    st16_nt(dst + 8 * i, valid < kPageTokens ? mask_tail<D>(x[j], i, valid) : x[j]);
   }
 }
 
@@ -131,11 +131,11 @@ __global__ __launch_bounds__(64) void kv_unpack_kernel(const uint16_t* __restric
   const int valid = rem < kPageTokens ? static_cast<int>(rem) : kPageTokens;
   uint4 x[kPerLane];
 #pragma unroll
-  for (int j = 0; j < kPerLane; ++j) x[j] = ld16(src + 8 * (threadIdx.x + 64 * j));
+  for (int j = 0; j < kPerLane; ++j) x[j] = ld16_nt(src + 8 * (threadIdx.x + 64 * j));
 #pragma unroll
   for (int j = 0; j < kPerLane; ++j) {
     const int i = threadIdx.x + 64 * j;
-    st16(dst + 8 * i, valid < kPageTokens ? mask_tail<D>(x[j], i, valid) : x[j]);
+    st16_nt(dst + 8 * i, valid < kPageTokens ? mask_tail<D>(x[j], i, valid) : x[j]);
   }
   if (blockIdx.y == 0 && threadIdx.x == 0) pt_row[lp] = page;
 }
