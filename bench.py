@@ -474,6 +474,41 @@ def bench_prefill_transfer(args):
 
 
 # ------------------------------------------------------------------------------------------------
+# prefill latency curve (the placement layer's admission signal, Section 3.1 / 4.2)
+# ------------------------------------------------------------------------------------------------
+def bench_prefill_curve(args):
+    """Turn-1 prefill time of one conversation against its length (32q/8kv, d 128, one layer), the
+    quadratic least-squares fit the scheduler reads at admission (cs_prefill_curve_fit) and its
+    R^2. The paper profiles the same curve offline on its prefiller and finds it quadratic with
+    R^2 = 1.0 (Section 3.1)."""
+    from paper_2606_01839_amd import KVPool, prefill_curve_fit
+    hq, hkv, d, seed = 32, 8, 128, 1006
+    lens = [2048, 4096, 8192, 16384, 32768, 65536, 131072]
+    pool = KVPool(1, hq, hkv, d, n_pages=pages_for(max(lens)) + 8, max_convs=2,
+                  max_pages_per_conv=pages_for(max(lens)), placement_seed=seed)
+    ms = []
+    for L in lens:
+        c = pool.conv_create()
+        k, v = gen_kv(seed, 0, 0, L, hkv, d)
+        pool.kv_append(c, k[None], v[None])
+        q = gen_q(seed, 0, 0, L, hq, d)
+        out = torch.empty_like(q)
+        step = lambda: pool.attn_prefill_turn1([c], [L], 0, q, out)
+        step()
+        prof = profiled(pool, step, 2)
+        ms.append(prof["attn_fwd"][0] / prof["attn_fwd"][1])
+        pool.conv_destroy(c)
+        del k, v, q, out
+    pool.close()
+    torch.cuda.empty_cache()
+    coef, r2 = prefill_curve_fit(lens, [m * 1e-3 for m in ms])
+    return {"prefill_curve": {
+        "workload": "turn-1 prefill of one conversation, 32q/8kv, d 128, 1 layer, L in " + str(lens),
+        "lengths": lens, "kernel_ms": ms, "coef_s": list(coef), "r2": r2,
+        "tflops": [attn_flops([0], [L], hq, d) / (m * 1e-3) / 1e12 for L, m in zip(lens, ms)]}}
+
+
+# ------------------------------------------------------------------------------------------------
 # mixed agentic trace (256 conversations, 32 layers, Llama-3-8B attention shape)
 # ------------------------------------------------------------------------------------------------
 class _Live:
@@ -694,7 +729,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--skip-components", action="store_true")
-    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed"], default=None,
+    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed", "curve"], default=None,
                     help="run one component and print only its JSON (for profiling)")
     ap.add_argument("--mixed-steps", type=int, default=300,
                     help="timed steps of the mixed agentic trace component (0 = skip it)")
@@ -714,7 +749,8 @@ def main():
     if args.calibrate_copy:
         copy_calibration()
     if args.only and args.only != "decode":
-        fn = {"extend": bench_extend, "prefill": bench_prefill_transfer, "mixed": bench_mixed}[args.only]
+        fn = {"extend": bench_extend, "prefill": bench_prefill_transfer, "mixed": bench_mixed,
+              "curve": bench_prefill_curve}[args.only]
         print(json.dumps({"component": args.only, **fn(args)}), flush=True)
         return
     dec = bench_decode(args)
@@ -722,6 +758,7 @@ def main():
     if not args.skip_components and not args.only:
         comps.update(bench_extend(args))
         comps.update(bench_prefill_transfer(args))
+        comps.update(bench_prefill_curve(args))
         if args.mixed_steps > 0:
             comps.update(bench_mixed(args))
     split_gbs = dec["split_bytes"] / (dec["split_ms"] * 1e-3) / 1e9

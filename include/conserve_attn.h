@@ -53,7 +53,8 @@ enum {
   CS_ENOENT = -3,  /* unknown or destroyed conversation handle */
   CS_ESTATE = -4,  /* call not valid in the conversation's state (e.g. q_len > length) */
   CS_ERANGE = -5,  /* index out of range (layer, page capacity of a conversation) */
-  CS_EHIP = -6     /* a HIP runtime call failed */
+  CS_EHIP = -6,    /* a HIP runtime call failed */
+  CS_EBUSY = -7    /* placement refused: the prefiller is saturated (conserve_sched.h) */
 };
 
 #define CS_PAGE_TOKENS 16

@@ -15,9 +15,10 @@ import torch
 
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libconserve_attn.so")
 
-CS_OK, CS_EINVAL, CS_ENOMEM, CS_ENOENT, CS_ESTATE, CS_ERANGE, CS_EHIP = 0, -1, -2, -3, -4, -5, -6
+CS_OK, CS_EINVAL, CS_ENOMEM, CS_ENOENT, CS_ESTATE, CS_ERANGE, CS_EHIP, CS_EBUSY = 0, -1, -2, -3, -4, -5, -6, -7
 STATUS_NAMES = {CS_EINVAL: "CS_EINVAL", CS_ENOMEM: "CS_ENOMEM", CS_ENOENT: "CS_ENOENT",
-                CS_ESTATE: "CS_ESTATE", CS_ERANGE: "CS_ERANGE", CS_EHIP: "CS_EHIP"}
+                CS_ESTATE: "CS_ESTATE", CS_ERANGE: "CS_ERANGE", CS_EHIP: "CS_EHIP",
+                CS_EBUSY: "CS_EBUSY"}
 PAGE_TOKENS = 16
 
 EXPORTS = [
@@ -27,6 +28,10 @@ EXPORTS = [
     "cs_attn_decode_batch", "cs_mixed_step", "cs_kv_pack_size", "cs_kv_pack", "cs_kv_unpack",
     "cs_profile_start",
     "cs_profile_stop", "cs_last_error",
+    # placement layer (include/conserve_sched.h)
+    "cs_prefill_curve_fit", "cs_prefill_curve_eval", "cs_provision_decoders",
+    "cs_place_least_occupied", "cs_sched_create", "cs_sched_destroy", "cs_sched_admit",
+    "cs_sched_bind",
 ]
 PROFILE_KINDS = ["append", "pack", "unpack", "decode_split", "decode_merge", "attn_fwd"]
 
@@ -42,6 +47,10 @@ class PoolDesc(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("max_convs", ctypes.c_int32), ("max_pages_per_conv", ctypes.c_int32),
                 ("n_pages", ctypes.c_int64)]
+
+
+class PrefillCurve(ctypes.Structure):
+    _fields_ = [("c0", ctypes.c_double), ("c1", ctypes.c_double), ("c2", ctypes.c_double)]
 
 
 _lib = None
@@ -81,6 +90,17 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "cs_profile_start": (I32, [P]),
         "cs_profile_stop": (I32, [P, ctypes.POINTER(ctypes.c_double), PI64]),
         "cs_last_error": (ctypes.c_char_p, []),
+        "cs_prefill_curve_fit": (I32, [I32, PI64, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(PrefillCurve), ctypes.POINTER(ctypes.c_double)]),
+        "cs_prefill_curve_eval": (I32, [ctypes.POINTER(PrefillCurve), I64, ctypes.POINTER(ctypes.c_double)]),
+        "cs_provision_decoders": (I32, [ctypes.c_double] * 6 + [ctypes.POINTER(ctypes.c_double)] * 3 + [PI32]),
+        "cs_place_least_occupied": (I32, [I32, PI64, PI64, I64, PI32]),
+        "cs_sched_create": (I32, [ctypes.POINTER(PrefillCurve), ctypes.c_double, I32, ctypes.POINTER(P),
+                                  ctypes.POINTER(P)]),
+        "cs_sched_destroy": (I32, [P]),
+        "cs_sched_admit": (I32, [P, I64, ctypes.c_double, ctypes.POINTER(ctypes.c_double),
+                                 ctypes.POINTER(ctypes.c_double)]),
+        "cs_sched_bind": (I32, [P, I64, PI32]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -325,3 +345,104 @@ class KVPool:
         _check(self.lib.cs_kv_unpack(self._handle, src.data_ptr(), src.numel() * src.element_size(),
                                      n_tokens, ctypes.byref(c), _stream_handle(self.device)))
         return c.value
+
+
+# ------------------------------------------------------------------------------------------------
+# placement layer (include/conserve_sched.h)
+# ------------------------------------------------------------------------------------------------
+def prefill_curve_fit(tokens, seconds):
+    """Least-squares quadratic t(L) = c0 + c1 L + c2 L^2; returns ((c0, c1, c2), r2)."""
+    lib = load_library()
+    t = np.ascontiguousarray(np.asarray(tokens, dtype=np.int64).reshape(-1))
+    y = np.ascontiguousarray(np.asarray(seconds, dtype=np.float64).reshape(-1))
+    if t.size != y.size:
+        raise ValueError("tokens and seconds differ in length")
+    c, r2 = PrefillCurve(), ctypes.c_double()
+    _check(lib.cs_prefill_curve_fit(int(t.size), t.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                    y.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                    ctypes.byref(c), ctypes.byref(r2)))
+    return (c.c0, c.c1, c.c2), r2.value
+
+
+def prefill_curve_eval(coef, tokens: int) -> float:
+    lib = load_library()
+    c, out = PrefillCurve(*coef), ctypes.c_double()
+    _check(lib.cs_prefill_curve_eval(ctypes.byref(c), int(tokens), ctypes.byref(out)))
+    return out.value
+
+
+def provision_decoders(prefill_tokens_per_s, mean_turn1_tokens, decoder_tokens_per_s,
+                       mean_decoder_tokens, convs_per_decoder, mean_lifetime_s):
+    """Section 4.1 sizing; returns dict(saturation_rate, n_throughput, n_memory, n_decoders)."""
+    lib = load_library()
+    r, a, b = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    n = ctypes.c_int32()
+    _check(lib.cs_provision_decoders(float(prefill_tokens_per_s), float(mean_turn1_tokens),
+                                     float(decoder_tokens_per_s), float(mean_decoder_tokens),
+                                     float(convs_per_decoder), float(mean_lifetime_s),
+                                     ctypes.byref(r), ctypes.byref(a), ctypes.byref(b), ctypes.byref(n)))
+    return {"saturation_rate": r.value, "n_throughput": a.value, "n_memory": b.value,
+            "n_decoders": n.value}
+
+
+def place_least_occupied(used_pages, free_pages, need_pages: int) -> int:
+    """Index of the decoder the binding rule picks, or -1 (CS_ENOMEM) when none fits."""
+    lib = load_library()
+    u = np.ascontiguousarray(np.asarray(used_pages, dtype=np.int64).reshape(-1))
+    f = np.ascontiguousarray(np.asarray(free_pages, dtype=np.int64).reshape(-1))
+    if u.size != f.size:
+        raise ValueError("used_pages and free_pages differ in length")
+    d = ctypes.c_int32()
+    code = lib.cs_place_least_occupied(int(u.size), u.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                       f.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                       int(need_pages), ctypes.byref(d))
+    if code == CS_ENOMEM:
+        return -1
+    _check(code)
+    return d.value
+
+
+class Scheduler:
+    """Reactive conversation placement over decoder KVPools (cs_sched_*). The pools stay owned
+    by the caller and must outlive the scheduler."""
+
+    def __init__(self, coef, max_wait_s: float, decoders):
+        self.lib = load_library()
+        self.decoders = list(decoders)
+        arr = (ctypes.c_void_p * len(self.decoders))(*[d._handle for d in self.decoders])
+        c = PrefillCurve(*coef)
+        h = ctypes.c_void_p()
+        _check(self.lib.cs_sched_create(ctypes.byref(c), float(max_wait_s), len(self.decoders),
+                                        ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)),
+                                        ctypes.byref(h)))
+        self._handle = h
+
+    def admit(self, turn1_tokens: int, now_s: float):
+        """(start_s, done_s) of the turn-1 prefill, or None when refused (CS_EBUSY)."""
+        a, b = ctypes.c_double(), ctypes.c_double()
+        code = self.lib.cs_sched_admit(self._handle, int(turn1_tokens), float(now_s),
+                                       ctypes.byref(a), ctypes.byref(b))
+        if code == CS_EBUSY:
+            return None
+        _check(code)
+        return a.value, b.value
+
+    def bind(self, kv_tokens: int) -> int:
+        """Decoder index for a conversation of kv_tokens tokens, or -1 (CS_ENOMEM)."""
+        d = ctypes.c_int32()
+        code = self.lib.cs_sched_bind(self._handle, int(kv_tokens), ctypes.byref(d))
+        if code == CS_ENOMEM:
+            return -1
+        _check(code)
+        return d.value
+
+    def close(self) -> None:
+        if self._handle:
+            _check(self.lib.cs_sched_destroy(self._handle))
+            self._handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

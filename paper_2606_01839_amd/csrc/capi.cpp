@@ -773,3 +773,7 @@ cs_status cs_profile_stop(cs_pool* p, double* ms, int64_t* launches) {
 }
 
 }  // extern "C"
+namespace cs {
+// Error reporting shared with the other C-ABI translation units (sched_capi.cpp).
+cs_status api_fail(cs_status code, const char* msg) { return fail(code, msg); }
+}  // namespace cs

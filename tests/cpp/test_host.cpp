@@ -1,12 +1,14 @@
 // Host-metadata unit test (page pool, conversation table, plans); built with -fsanitize=address,
 // undefined by tests/test_host_cpp.py. Exits non-zero on the first failed check.
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <set>
 #include <vector>
 
 #include "host/host_state.hpp"
+#include "host/sched.hpp"
 
 #define CHECK(c)                                                          \
   do {                                                                    \
@@ -91,7 +93,39 @@ static void append_plan() {
   CHECK(ch[3].conv == 1 && ch[3].lpage == 0 && ch[3].t0 == 0 && ch[3].t1 == 16 && ch[3].src_row == 30 && ch[3].new_page);
 }
 
+static void placement() {
+  // binding: fraction of pages used, exact for counts near 2^62 (no overflow under UBSan)
+  const int64_t big = int64_t(1) << 61;
+  int64_t used[3] = {big - 1, big - 2, 5}, fr[3] = {big + 1, big + 2, 0};
+  CHECK(cs::least_occupied(3, used, fr, 1) == 1);
+  CHECK(cs::least_occupied(3, used, fr, big + 2) == 1);
+  CHECK(cs::least_occupied(3, used, fr, big + 3) == -1);
+  // curve fit: exact quadratic recovered; degenerate inputs refused
+  int64_t L[4] = {1000, 2000, 4000, 8000};
+  double t[4];
+  for (int i = 0; i < 4; ++i) t[i] = 0.5 + 2e-4 * L[i] + 3e-8 * double(L[i]) * L[i];
+  cs::PrefillCurve c;
+  double r2 = 0;
+  CHECK(cs::fit_prefill_curve(L, t, 4, &c, &r2));
+  CHECK(std::fabs(c.c0 - 0.5) < 1e-9 && std::fabs(c.c1 - 2e-4) < 1e-12 && std::fabs(c.c2 - 3e-8) < 1e-15);
+  CHECK(std::fabs(r2 - 1.0) < 1e-12);
+  int64_t same[3] = {7, 7, 9};
+  CHECK(!cs::fit_prefill_curve(same, t, 3, &c, &r2));
+  // provisioning and admission
+  cs::Provisioning p;
+  CHECK(cs::provision_decoders(25000, 15000, 1000, 1000, 1e9, 1, &p) && p.n_decoders == 2);
+  CHECK(!cs::provision_decoders(0, 1, 1, 1, 1, 1, &p));
+  cs::PrefillCurve one;
+  one.c0 = 1.0;
+  cs::Admission a(one, 1.5);
+  double st = 0, dn = 0;
+  CHECK(a.admit(10, 0.0, &st, &dn) && st == 0.0 && dn == 1.0);
+  CHECK(a.admit(10, 0.2, &st, &dn) && st == 1.0 && dn == 2.0);
+  CHECK(!a.admit(10, 0.4, &st, &dn) && a.busy_until() == 2.0);
+}
+
 int main() {
+  placement();
   pool_basics();
   conv_table();
   decode_plan();

@@ -1,4 +1,4 @@
-"""CPU: the HIP-free host metadata layer (page pool, conversation table, work plans) built with
+"""CPU: the HIP-free host layer (page pool, conversation table, work plans, placement) built with
 g++ -fsanitize=address,undefined and run."""
 import os
 import shutil
@@ -18,7 +18,8 @@ def test_host_metadata_under_sanitizers():
         cmd = ["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined",
                "-fno-sanitize-recover=all", "-I", CSRC,
                os.path.join(ROOT, "tests", "cpp", "test_host.cpp"),
-               os.path.join(CSRC, "host", "host_state.cpp"), "-o", exe]
+               os.path.join(CSRC, "host", "host_state.cpp"), os.path.join(CSRC, "host", "sched.cpp"),
+               "-o", exe]
         r = subprocess.run(cmd, capture_output=True, text=True)
         assert r.returncode == 0, r.stderr
         r = subprocess.run([exe], capture_output=True, text=True, timeout=120,
