@@ -508,6 +508,41 @@ def bench_prefill_curve(args):
         "tflops": [attn_flops([0], [L], hq, d) / (m * 1e-3) / 1e12 for L, m in zip(lens, ms)]}}
 
 
+def bench_gqa_shapes(args):
+    """The same attention kernel at the GQA shape of the paper's served model (Qwen3-0.6B: 16 query
+    heads, 8 KV heads, head_dim 128; Section 5.1) beside the Llama-3-8B shape (32/8/128): turn-1
+    prefill of 4 conversations of 32k-64k tokens, one layer."""
+    from paper_2606_01839_amd import KVPool
+    res = {}
+    lens = np.array([32768, 65536, 49152, 40960])
+    for hq, hkv in [(16, 8), (32, 8)]:
+        d, seed = 128, 1007
+        pool = KVPool(1, hq, hkv, d, n_pages=int(sum(pages_for(int(L)) for L in lens)) + 16,
+                      max_convs=len(lens), max_pages_per_conv=pages_for(int(lens.max())),
+                      placement_seed=seed)
+        convs = []
+        for b, L in enumerate(lens):
+            c = pool.conv_create()
+            k, v = gen_kv(seed, b, 0, int(L), hkv, d)
+            pool.kv_append(c, k[None], v[None])
+            convs.append(c)
+            del k, v
+        q = torch.cat([gen_q(seed, b, 0, int(L), hq, d) for b, L in enumerate(lens)])
+        out = torch.empty_like(q)
+        step = lambda: pool.attn_prefill_turn1(convs, lens, 0, q, out)
+        step()
+        prof = profiled(pool, step, 2)
+        ms = prof["attn_fwd"][0] / prof["attn_fwd"][1]
+        fl = attn_flops([0] * len(lens), lens, hq, d)
+        res[f"{hq}q/{hkv}kv"] = {"kernel_ms": ms, "tflops": fl / (ms * 1e-3) / 1e12,
+                                 "frac": fl / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS}
+        pool.close()
+        del q, out
+        torch.cuda.empty_cache()
+    return {"gqa_shapes": {"workload": "turn-1 prefill, 4 conversations of 32k-64k tokens, d 128, 1 layer",
+                           **res}}
+
+
 # ------------------------------------------------------------------------------------------------
 # mixed agentic trace (256 conversations, 32 layers, Llama-3-8B attention shape)
 # ------------------------------------------------------------------------------------------------
@@ -729,7 +764,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--skip-components", action="store_true")
-    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed", "curve"], default=None,
+    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed", "curve", "shapes"], default=None,
                     help="run one component and print only its JSON (for profiling)")
     ap.add_argument("--mixed-steps", type=int, default=300,
                     help="timed steps of the mixed agentic trace component (0 = skip it)")
@@ -750,7 +785,7 @@ def main():
         copy_calibration()
     if args.only and args.only != "decode":
         fn = {"extend": bench_extend, "prefill": bench_prefill_transfer, "mixed": bench_mixed,
-              "curve": bench_prefill_curve}[args.only]
+              "curve": bench_prefill_curve, "shapes": bench_gqa_shapes}[args.only]
         print(json.dumps({"component": args.only, **fn(args)}), flush=True)
         return
     dec = bench_decode(args)
@@ -759,6 +794,7 @@ def main():
         comps.update(bench_extend(args))
         comps.update(bench_prefill_transfer(args))
         comps.update(bench_prefill_curve(args))
+        comps.update(bench_gqa_shapes(args))
         if args.mixed_steps > 0:
             comps.update(bench_mixed(args))
     split_gbs = dec["split_bytes"] / (dec["split_ms"] * 1e-3) / 1e9

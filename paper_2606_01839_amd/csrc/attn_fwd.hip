@@ -1,7 +1,8 @@
 // Turn-1 prefill and turn-N extend-prefill attention over paged KV (flash-attention forward).
 //
-// A workgroup owns one (conversation, 64-query block, kv head) tile; its waves cover the G query
-// heads of that kv head (the GQA group), so every K/V tile in LDS serves 64*G query rows.
+// A workgroup owns one (conversation, query block, kv head) tile; its waves cover the G query
+// heads of that kv head (the GQA group), so every K/V tile in LDS serves all the query rows of
+// the group (256 rows at head_dim 128).
 // Each wave computes the transposed score tile on the matrix cores (v_mfma_f32_32x32x16_bf16):
 //   S^T[key][query] = K[key][:] . Q[query][:]       A = K rows from LDS, B = Q kept in registers
 //   O^T[dim][query] += V^T[dim][key] . P^T[key][query]   A = V^T rows from LDS, B = P registers
@@ -10,7 +11,8 @@
 // one exchange between the halves, and the P accumulator registers are directly the B operand of
 // the PV product: the key order of K or V^T in LDS is arranged so the two contractions agree.
 //
-// head_dim 128 (attn_fwd_kernel): two waves per query head (32 queries each), two waves per SIMD.
+// head_dim 128 (attn_fwd_kernel): eight waves, G query heads x 8/G blocks of 32 queries (a 64-query
+// tile at G = 4, 128 queries at G = 2), two waves per SIMD.
 // K/V tiles of 64 keys (4 pages) are copied from HBM straight into a four-deep LDS ring with
 // global_load_lds_dwordx4 (no staging registers, no LDS store instructions), three tiles ahead;
 // the K operands of tile j+1 are read into registers while the PV product of tile j runs.
@@ -39,7 +41,7 @@ struct ExtendArgs {
 };
 
 constexpr int kBN = 64;  // keys per tile
-constexpr int kBM = 64;  // query tokens per workgroup
+constexpr int kBM = 64;  // query tokens per workgroup of the head_dim 64 kernel
 
 // LDS tile of the staged kernel (padded rows: bank-conflict-free MFMA operand reads).
 template <int D>
@@ -89,10 +91,12 @@ __device__ __forceinline__ void dma_wait_barrier() {
 }
 
 template <int G>
-__global__ __launch_bounds__(64 * G * (kBM / 32)) __attribute__((amdgpu_waves_per_eu(G >= 4 ? 2 : 1)))
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_fwd_kernel(ExtendArgs a) {
   constexpr int D = 128;
-  constexpr int NW = G * (kBM / 32);
+  constexpr int NW = 8;                   // waves: G query heads x (8 / G) blocks of 32 queries
+  constexpr int BM = 32 * (NW / G);       // queries per workgroup
+  static_assert(NW % G == 0, "the group must divide the eight waves");
   constexpr int KS = D / 16;
   constexpr int DT = D / 32;
   constexpr int NB = 16;                  // 1 KiB blocks per K (and per V^T) tile
@@ -107,7 +111,7 @@ void attn_fwd_kernel(ExtendArgs a) {
   const ExtendTile tile = a.tiles[tile_idx];
   const ExtendConvDesc cd = a.convs[tile.conv];
   const int prefix = cd.len - cd.q_len;
-  const int q_hi = min(cd.q_len, tile.q0 + kBM);
+  const int q_hi = min(cd.q_len, tile.q0 + BM);
   const int pos_min = prefix + tile.q0, pos_max = prefix + q_hi - 1;
   const int n_kt = pos_max / kBN + 1;
   const int n_pg = (cd.len + kPageTokens - 1) / kPageTokens;
@@ -571,18 +575,18 @@ void attn_fwd_staged_kernel(ExtendArgs a) {
   }
 }
 
-// head_dim 128: 32 queries per wave, 2G waves (two per SIMD at G = 4); head_dim 64: 64 queries
+// head_dim 128: 32 queries per wave, eight waves (two per SIMD); head_dim 64: 64 queries
 // per wave, G waves.
 template <int D, int G>
 static void launch_fwd(const ExtendArgs& a, int n_tiles, int n_kv_heads, hipStream_t stream) {
   if constexpr (D == 128) {
-    attn_fwd_kernel<G><<<n_tiles * n_kv_heads, 64 * G * (kBM / 32), 0, stream>>>(a);
+    attn_fwd_kernel<G><<<n_tiles * n_kv_heads, 512, 0, stream>>>(a);
   } else {
     attn_fwd_staged_kernel<D, G, 2, kBM><<<n_tiles * n_kv_heads, 64 * G * (kBM / 64), 0, stream>>>(a);
   }
 }
 
-int extend_query_tile(int) { return kBM; }
+int extend_query_tile(int head_dim, int group) { return head_dim == 128 ? 256 / group : kBM; }
 
 hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,
                          const ExtendTile* d_tiles, int n_tiles, const void* q, void* out,

@@ -41,8 +41,9 @@ hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDes
 hipError_t launch_decode_merge(const PoolGeom& g, const DecodeConvDesc* d_convs, int n_convs,
                                const float* partials, void* out, hipStream_t stream);
 
-// Query tokens per extend/prefill work tile for this head size (the host plan must match).
-int extend_query_tile(int head_dim);
+// Query tokens per extend/prefill work tile for this head size and GQA group (the host plan must
+// match).
+int extend_query_tile(int head_dim, int group);
 
 // Extend / prefill: one workgroup per (tile, kv head).
 hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,

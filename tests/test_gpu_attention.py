@@ -58,7 +58,7 @@ def test_prefill_turn1_ragged(hq, hkv, d):
     _extend_case(hq, hkv, d, [0, 0, 0, 0, 0], [1, 17, 64, 130, 333])
 
 
-@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (4, 2, 64)])
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (16, 8, 128), (4, 2, 64)])
 def test_extend_against_prefix(hq, hkv, d):
     _extend_case(hq, hkv, d, [1, 15, 64, 100, 1000, 2047], [1, 64, 65, 127, 200, 77])
 
@@ -151,11 +151,13 @@ def test_chunked_extend_matches_one_shot_prefill():
     pool.close()
 
 
-def test_aligned_chunked_prefill_is_bitwise_one_shot():
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (16, 8)])
+def test_aligned_chunked_prefill_is_bitwise_one_shot(hq, hkv):
     """Chunked turn-1 prefill (the prefiller's chunked prefill, Section 5.1) with chunks that are
-    multiples of the 64-query tile: every query tile sweeps the same key tiles in the same order as
-    in the one-shot prefill, so the outputs agree bit for bit (and both match the oracle)."""
-    hq, hkv, d = 32, 8, 128
+    multiples of the query tile (64 queries at 32q/8kv, 128 at 16q/8kv): every query tile sweeps
+    the same key tiles in the same order as in the one-shot prefill, so the outputs agree bit for
+    bit (and both match the oracle)."""
+    d = 128
     lens, chunk = [700, 300], 256
     pool = _pool(hq, hkv, d, 2 * sum((L + 15) // 16 for L in lens) + 8)
     one = [pool.conv_create() for _ in lens]
