@@ -510,12 +510,12 @@ def bench_prefill_curve(args):
 
 def bench_gqa_shapes(args):
     """The same attention kernel at the GQA shape of the paper's served model (Qwen3-0.6B: 16 query
-    heads, 8 KV heads, head_dim 128; Section 5.1) beside the Llama-3-8B shape (32/8/128): turn-1
-    prefill of 4 conversations of 32k-64k tokens, one layer."""
+    heads, 8 KV heads, head_dim 128; Section 5.1), the Llama-3-8B shape (32/8/128) and a group of 8
+    (64/8/128): turn-1 prefill of 4 conversations of 32k-64k tokens, one layer."""
     from paper_2606_01839_amd import KVPool
     res = {}
     lens = np.array([32768, 65536, 49152, 40960])
-    for hq, hkv in [(16, 8), (32, 8)]:
+    for hq, hkv in [(16, 8), (32, 8), (64, 8)]:
         d, seed = 128, 1007
         pool = KVPool(1, hq, hkv, d, n_pages=int(sum(pages_for(int(L)) for L in lens)) + 16,
                       max_convs=len(lens), max_pages_per_conv=pages_for(int(lens.max())),

@@ -610,7 +610,7 @@ hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_c
     launch_fwd<DD, GG>(a, n_tiles, g.n_kv_heads, stream);     \
     return hipGetLastError();                                 \
   }
-  CS_FWD_CASE(128, 2) CS_FWD_CASE(128, 4)
+  CS_FWD_CASE(128, 1) CS_FWD_CASE(128, 2) CS_FWD_CASE(128, 4) CS_FWD_CASE(128, 8)
   CS_FWD_CASE(64, 1) CS_FWD_CASE(64, 2) CS_FWD_CASE(64, 4) CS_FWD_CASE(64, 8)
 #undef CS_FWD_CASE
   return hipErrorInvalidValue;

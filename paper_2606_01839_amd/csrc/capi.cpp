@@ -62,10 +62,8 @@ const char* desc_problem(const cs_pool_desc* d) {
     return "n_q_heads must be a positive multiple of n_kv_heads";
   const int group = d->n_q_heads / d->n_kv_heads;
   if (d->head_dim != 64 && d->head_dim != 128) return "head_dim must be 64 or 128";
-  if (d->head_dim == 128 && group != 2 && group != 4)
-    return "head_dim 128 supports n_q_heads/n_kv_heads in {2, 4}";
-  if (d->head_dim == 64 && group != 1 && group != 2 && group != 4 && group != 8)
-    return "head_dim 64 supports n_q_heads/n_kv_heads in {1, 2, 4, 8}";
+  if (group != 1 && group != 2 && group != 4 && group != 8)
+    return "n_q_heads/n_kv_heads must be 1, 2, 4 or 8";
   if (d->max_convs < 1 || d->max_convs > (1 << cs::ConvTable::kSlotBits))
     return "max_convs must be in [1, 2^20]";
   if (d->max_pages_per_conv < 1 || d->max_pages_per_conv > (1 << 26))

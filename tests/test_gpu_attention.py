@@ -53,12 +53,13 @@ def _extend_case(hq, hkv, d, prefixes, chunks, pool_seed=3, scales=(None, None))
     return out
 
 
-@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (4, 2, 64), (16, 8, 128), (8, 1, 64), (4, 4, 64)])
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (4, 2, 64), (16, 8, 128), (64, 8, 128), (8, 8, 128),
+                                      (8, 1, 64), (4, 4, 64)])
 def test_prefill_turn1_ragged(hq, hkv, d):
     _extend_case(hq, hkv, d, [0, 0, 0, 0, 0], [1, 17, 64, 130, 333])
 
 
-@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (16, 8, 128), (4, 2, 64)])
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (16, 8, 128), (64, 8, 128), (4, 2, 64)])
 def test_extend_against_prefix(hq, hkv, d):
     _extend_case(hq, hkv, d, [1, 15, 64, 100, 1000, 2047], [1, 64, 65, 127, 200, 77])
 
@@ -88,7 +89,8 @@ def _decode_case(hq, hkv, d, lens, pool_seed=3, scales=(None, None)):
     return res, q
 
 
-@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (4, 2, 64), (8, 8, 64), (16, 8, 128)])
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (4, 2, 64), (8, 8, 64), (16, 8, 128), (64, 8, 128),
+                                      (8, 8, 128)])
 def test_decode_ragged(hq, hkv, d):
     _decode_case(hq, hkv, d, [1, 2, 15, 16, 17, 31, 32, 33, 100, 511, 512, 513, 1024, 1025, 3000])
 
