@@ -312,7 +312,8 @@ struct ExtendWork {
 
 cs_status upload_extend(cs_pool* p, const std::vector<int32_t>& slots, const std::vector<int64_t>& lens,
                         const std::vector<int32_t>& q_lens, ExtendWork* w) {
-  cs::ExtendPlan plan = cs::plan_extend(slots, lens, q_lens, cs::extend_query_tile(p->desc.head_dim, p->desc.n_q_heads / p->desc.n_kv_heads));
+  const int tile = cs::extend_query_tile(p->desc.head_dim, p->desc.n_q_heads / p->desc.n_kv_heads);
+  cs::ExtendPlan plan = cs::plan_extend(slots, lens, q_lens, tile);
   const size_t desc_bytes = align_up(plan.convs.size() * sizeof(cs::ExtendConvDesc), 16);
   if (desc_bytes + kAlign + sizeof(cs::ExtendTile) > kQuarter)
     return fail(CS_ENOMEM, "batch descriptor exceeds the metadata ring");

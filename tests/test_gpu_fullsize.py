@@ -109,3 +109,43 @@ def test_turn1_prefill_full_size_sampled_rows():
         del k, v, kf, vf
     assert_close(torch.cat(got), np.concatenate(ref), "turn-1 prefill, sampled rows of 8 conversations")
     pool.close()
+
+
+def test_turn1_transfer_full_size_bit_exact():
+    """The one-time transfer of the whole turn-1 batch (8 conversations, 32k-128k tokens): pack ->
+    unpack into a pool with another placement -> pack again is byte-identical; the destination's
+    page tables are valid; sampled wire pages equal the oracle's serialization of the generator's
+    tokens (first, second, last two and seeded random pages of every conversation)."""
+    from oracle import kvwire
+    from paper_2606_01839_amd import KVPool
+    tr = PrefillTransfer()
+    sh = tr.shape
+    hkv, d = sh.n_kv_heads, sh.head_dim
+    pool, convs, lens, q = bench.make_prefill_case(tr)
+    del q
+    wires = [pool.kv_pack(c) for c in convs]
+    dst = KVPool(1, sh.n_q_heads, hkv, d, n_pages=pool.desc.n_pages, max_convs=tr.n_convs,
+                 max_pages_per_conv=bench.pages_for(tr.hi), placement_seed=tr.dst_seed)
+    dconvs = [dst.kv_unpack(w, int(L)) for w, L in zip(wires, lens)]
+    torch.cuda.synchronize()
+    seen = set()
+    for c, w, L in zip(dconvs, wires, lens):
+        assert torch.equal(dst.kv_pack(c), w)
+        pages = dst.conv_pages(c)
+        assert len(pages) == bench.pages_for(int(L)) and all(0 <= p < dst.desc.n_pages for p in pages)
+        assert not (seen & set(pages))
+        seen |= set(pages)
+    assert dst.occupancy()[0] == len(seen)
+    rng = np.random.default_rng(3)
+    block = hkv * 2 * 16 * d                       # uint16 elements per logical page (one layer)
+    for b, (w, L) in enumerate(zip(wires, lens)):
+        L = int(L)
+        n_pg = bench.pages_for(L)
+        wire = w.cpu().numpy().view(np.uint16)
+        for p in sorted({0, 1, n_pg - 2, n_pg - 1} | set(int(x) for x in rng.integers(0, n_pg, size=5))):
+            t0, t1 = 16 * p, min(L, 16 * p + 16)
+            k, v = bench.gen_kv(tr.seed, b, t0, t1 - t0, hkv, d, device="cpu")
+            want = kvwire.serialize(sv.bf16_bits(k)[None], sv.bf16_bits(v)[None])
+            assert np.array_equal(wire[p * block:(p + 1) * block], want), (b, p)
+    pool.close()
+    dst.close()
