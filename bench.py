@@ -543,6 +543,81 @@ def bench_gqa_shapes(args):
                            **res}}
 
 
+def bench_transfer_overlap(args):
+    """The decoder receiving a transferred conversation while it decodes (Section 4: the turn-1 KV
+    arrives once, then stays): the decode batch (64 conversations, 8k-32k) runs 20 steps on one
+    stream while another stream unpacks a 65,536-token conversation of a 32-layer Llama-3-8B-shaped
+    model (8 GiB wire) into a second pool, back to back. Reports each kernel's event-timed rate
+    alone and under the overlap."""
+    from paper_2606_01839_amd import KVPool
+    tr = DecodeBatch()
+    sh = tr.shape
+    hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    pool, convs, lens, kv_dev, q = make_decode_case(tr)
+    del kv_dev
+    out = torch.empty_like(q)
+    NL, L, seed = 32, 65536, 1008
+    mk = lambda s: KVPool(NL, hq, hkv, d, n_pages=pages_for(L) + 8, max_convs=2,
+                          max_pages_per_conv=pages_for(L) + 8, placement_seed=s)
+    src, dst = mk(seed), mk(seed + 1)
+    c = src.conv_create()
+    for l0 in range(0, L, 8192):
+        k = torch.stack([sv.bf16_tensor(sv.mix_key(seed, 0, KIND_K, l), (8192, hkv, d), start=l0 * hkv * d,
+                                        device="cuda") for l in range(NL)])
+        v = torch.stack([sv.bf16_tensor(sv.mix_key(seed, 0, KIND_V, l), (8192, hkv, d), start=l0 * hkv * d,
+                                        device="cuda") for l in range(NL)])
+        src.kv_append(c, k, v)
+        del k, v
+    wire = src.kv_pack(c)
+    src.close()
+    torch.cuda.synchronize()
+    dec_bytes = int(lens.sum()) * 2 * hkv * d * 2 + len(lens) * hq * d * 2 + int(sum(pages_for(int(x)) for x in lens)) * 4
+    move = 2 * L * NL * hkv * d * 2 * 2
+
+    def unpack_once():
+        h = dst.kv_unpack(wire, L)
+        dst.conv_destroy(h)
+
+    def run(decode_steps, unpacks):
+        sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+        pool.profile_start()
+        dst.profile_start()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        with torch.cuda.stream(sb):
+            for _ in range(unpacks):
+                unpack_once()
+        with torch.cuda.stream(sa):
+            for _ in range(decode_steps):
+                pool.attn_decode_batch(convs, 0, q, out)
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3
+        pd, pu = pool.profile_stop(), dst.profile_stop()
+        res = {"wall_ms": wall,
+               "hbm_gbs": (decode_steps * dec_bytes + unpacks * move) / (wall * 1e-3) / 1e9}
+        if decode_steps:
+            ms = pd["decode_split"][0] / pd["decode_split"][1]
+            res["decode_split_ms"], res["decode_split_gbs"] = ms, dec_bytes / (ms * 1e-3) / 1e9
+        if unpacks:
+            ms = pu["unpack"][0] / unpacks
+            res["unpack_ms"], res["unpack_gbs"] = ms, move / (ms * 1e-3) / 1e9
+        return res
+
+    run(2, 1)
+    alone_dec, alone_up = run(20, 0), run(0, 4)
+    both = run(20, 4)
+    pool.close()
+    dst.close()
+    del wire, q, out
+    torch.cuda.empty_cache()
+    return {"transfer_overlap": {
+        "workload": "decode batch (64 conversations, 8k-32k, 1 layer) on one stream; unpack of a "
+                    "65536-token 32-layer 32q/8kv d128 conversation (8 GiB wire) on another",
+        "decode_alone": alone_dec, "unpack_alone": alone_up, "overlapped": both,
+        "note": "per-kernel rates use each kernel's own event-timed duration, which includes the "
+                "time the two streams share the GPU; hbm_gbs = all algorithmic bytes / wall time"}}
+
+
 # ------------------------------------------------------------------------------------------------
 # mixed agentic trace (256 conversations, 32 layers, Llama-3-8B attention shape)
 # ------------------------------------------------------------------------------------------------
@@ -764,7 +839,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--skip-components", action="store_true")
-    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed", "curve", "shapes"], default=None,
+    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed", "curve", "shapes", "overlap"], default=None,
                     help="run one component and print only its JSON (for profiling)")
     ap.add_argument("--mixed-steps", type=int, default=300,
                     help="timed steps of the mixed agentic trace component (0 = skip it)")
@@ -785,7 +860,8 @@ def main():
         copy_calibration()
     if args.only and args.only != "decode":
         fn = {"extend": bench_extend, "prefill": bench_prefill_transfer, "mixed": bench_mixed,
-              "curve": bench_prefill_curve, "shapes": bench_gqa_shapes}[args.only]
+              "curve": bench_prefill_curve, "shapes": bench_gqa_shapes,
+              "overlap": bench_transfer_overlap}[args.only]
         print(json.dumps({"component": args.only, **fn(args)}), flush=True)
         return
     dec = bench_decode(args)
@@ -795,6 +871,7 @@ def main():
         comps.update(bench_prefill_transfer(args))
         comps.update(bench_prefill_curve(args))
         comps.update(bench_gqa_shapes(args))
+        comps.update(bench_transfer_overlap(args))
         if args.mixed_steps > 0:
             comps.update(bench_mixed(args))
     split_gbs = dec["split_bytes"] / (dec["split_ms"] * 1e-3) / 1e9
