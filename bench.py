@@ -229,6 +229,15 @@ def bench_decode(args):
 
     step = lambda: pool.attn_decode_batch(convs, 0, q, out)
     ms = timed(step, args.steps, args.warmup)
+    # per-step distribution: events on the stream the pool launches on (torch's current stream)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a_, b_ in evs:
+        a_.record()
+        step()
+        b_.record()
+    torch.cuda.synchronize()
+    step_ms = np.array([a_.elapsed_time(b_) for a_, b_ in evs])
     prof = profiled(pool, step, args.steps)
     en = energy_run(step) if args.energy else None
     split_ms = prof["decode_split"][0] / max(1, prof["decode_split"][1])
@@ -278,6 +287,7 @@ def bench_decode(args):
     traffic = traffic_per_launch(workload)
     res = {
         "ms_per_step": ms,
+        "step_ms_p10_p50_p90": [float(np.percentile(step_ms, x)) for x in (10, 50, 90)],
         "value_gbs": step_bytes / (ms * 1e-3) / 1e9,
         "split_ms": split_ms,
         "merge_ms": merge_ms,
@@ -897,6 +907,7 @@ def main():
                      "kernel_ms": round(dec["split_ms"], 4), "merge_kernel_ms": round(dec["merge_ms"], 4)},
         "cpu_baseline": dec["cpu"],
         "parity": dec["parity"],
+        "step_ms_p10_p50_p90": dec["step_ms_p10_p50_p90"],
         "energy": dec["energy"],
         "components": comps,
     }
