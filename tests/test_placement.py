@@ -76,6 +76,8 @@ def test_oracle_admission_hand_timeline():
     assert a.admit(100, 0.4) is None and a.busy_until == 2.0   # would wait 1.6 s > 1.5: refused
     assert a.admit(100, 0.6) == (2.0, 3.0)                 # wait exactly 1.4 s
     assert a.admit(100, 5.0) == (5.0, 6.0)                 # idle prefiller: starts on arrival
+    b = op.Admission((1.0, 0.0, 0.0), max_wait_s=1.0)
+    assert b.admit(10, 0.0) == (0.0, 1.0) and b.admit(10, 0.0) == (1.0, 2.0)   # wait == bound: admitted
 
 
 # ---- library vs oracle ------------------------------------------------------------------------
