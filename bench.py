@@ -628,6 +628,41 @@ def bench_transfer_overlap(args):
                 "time the two streams share the GPU; hbm_gbs = all algorithmic bytes / wall time"}}
 
 
+def bench_decode_curve(args):
+    """Decode step time against the batch's active KV tokens (Section 3.2: decode is memory-bound,
+    gated by KV-cache bandwidth; the paper finds iteration latency set by decode at 262,144 active
+    tokens): 32 conversations of equal length, 32q/8kv d128, one layer, active tokens 32k..2M.
+    A least-squares line t = a + b * tokens gives the fixed cost a and the marginal bandwidth
+    4096 B / b."""
+    from paper_2606_01839_amd import KVPool
+    hq, hkv, d, seed, B = 32, 8, 128, 1009, 32
+    per = [1024, 2048, 4096, 8192, 16384, 32768, 65536]
+    pool = KVPool(1, hq, hkv, d, n_pages=B * pages_for(max(per)) + 16, max_convs=B,
+                  max_pages_per_conv=pages_for(max(per)), placement_seed=seed)
+    convs = [pool.conv_create() for _ in range(B)]
+    have = 0
+    pts = []
+    for L in per:
+        for b, c in enumerate(convs):
+            k, v = gen_kv(seed, b, have, L - have, hkv, d)
+            pool.kv_append(c, k[None], v[None])
+        have = L
+        q = torch.cat([gen_q(seed, b, L - 1, 1, hq, d) for b in range(B)])
+        out = torch.empty_like(q)
+        step = lambda: pool.attn_decode_batch(convs, 0, q, out)
+        ms = timed(step, 20, 3)
+        pts.append((B * L, ms))
+    pool.close()
+    torch.cuda.empty_cache()
+    x = np.array([p[0] for p in pts], dtype=np.float64)
+    y = np.array([p[1] for p in pts], dtype=np.float64)
+    b_, a_ = np.polyfit(x, y, 1)
+    return {"decode_curve": {
+        "workload": f"decode step, {B} conversations of equal length, 32q/8kv d128, 1 layer",
+        "active_tokens": [int(v) for v in x], "step_ms": [float(v) for v in y],
+        "fixed_ms": float(a_), "marginal_gbs": 4096 / (b_ * 1e-3) / 1e9}}
+
+
 # ------------------------------------------------------------------------------------------------
 # mixed agentic trace (256 conversations, 32 layers, Llama-3-8B attention shape)
 # ------------------------------------------------------------------------------------------------
@@ -849,7 +884,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--skip-components", action="store_true")
-    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed", "curve", "shapes", "overlap"], default=None,
+    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed", "curve", "shapes", "overlap",
+                                           "dcurve"], default=None,
                     help="run one component and print only its JSON (for profiling)")
     ap.add_argument("--mixed-steps", type=int, default=300,
                     help="timed steps of the mixed agentic trace component (0 = skip it)")
@@ -871,7 +907,7 @@ def main():
     if args.only and args.only != "decode":
         fn = {"extend": bench_extend, "prefill": bench_prefill_transfer, "mixed": bench_mixed,
               "curve": bench_prefill_curve, "shapes": bench_gqa_shapes,
-              "overlap": bench_transfer_overlap}[args.only]
+              "overlap": bench_transfer_overlap, "dcurve": bench_decode_curve}[args.only]
         print(json.dumps({"component": args.only, **fn(args)}), flush=True)
         return
     dec = bench_decode(args)
@@ -882,6 +918,7 @@ def main():
         comps.update(bench_prefill_curve(args))
         comps.update(bench_gqa_shapes(args))
         comps.update(bench_transfer_overlap(args))
+        comps.update(bench_decode_curve(args))
         if args.mixed_steps > 0:
             comps.update(bench_mixed(args))
     split_gbs = dec["split_bytes"] / (dec["split_ms"] * 1e-3) / 1e9
