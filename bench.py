@@ -689,6 +689,10 @@ def bench_mixed(args):
     NL, hq, hkv, d = sh.n_layers, sh.n_q_heads, sh.n_kv_heads, sh.head_dim
     trace = tr.conversations()
     page_bytes = NL * hkv * 2 * 16 * d * 2                       # one page, all layers
+    import gc
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()                                     # earlier components' cached blocks
     free, _ = torch.cuda.mem_get_info()
     max_t1 = max(c.turn1 for c in trace)
     reserve = 3 * pages_for(max_t1) * page_bytes + (24 << 30)    # prefiller, wire, step buffers
