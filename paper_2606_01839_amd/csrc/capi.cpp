@@ -33,7 +33,7 @@ constexpr int64_t kDecodeTargetItems = 4096;     // work items a decode launch a
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct WsLayout {
-  size_t page_table, partials, ring, total;
+  size_t page_table, partials, partials2, ring, total;
   size_t partial_floats;
 };
 
@@ -50,7 +50,11 @@ WsLayout ws_layout(const cs_pool_desc& d) {
   w.partials = align_up(pt_bytes, kAlign);
   w.partial_floats =
       static_cast<size_t>(max_decode_items(d)) * d.n_kv_heads * group * cs::partial_floats(d.head_dim);
-  w.ring = align_up(w.partials + w.partial_floats * 4, kAlign);
+  // A multi-layer pool gets a second partial buffer: cs_mixed_step merges layer l while it splits
+  // layer l+1 in the same launch.
+  w.partials2 = align_up(w.partials + w.partial_floats * 4, kAlign);
+  const size_t second = d.n_layers > 1 ? w.partial_floats * 4 : 0;
+  w.ring = align_up(w.partials2 + second, kAlign);
   w.total = w.ring + kRingBytes;
   return w;
 }
@@ -123,6 +127,7 @@ struct cs_pool {
     return g;
   }
   float* partials() const { return reinterpret_cast<float*>(ws + lay.partials); }
+  float* partials2() const { return reinterpret_cast<float*>(ws + lay.partials2); }
 };
 
 namespace {
@@ -728,10 +733,30 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
                                   static_cast<char*>(out_ext) + off, ext_stream)) != CS_OK)
       break;
   }
-  for (int32_t layer = 0; layer < p->desc.n_layers && n_dec > 0 && st == CS_OK; ++layer) {
-    const size_t off = static_cast<size_t>(layer) * static_cast<size_t>(n_dec) * row_bytes;
-    st = launch_decode_layer(p, dw, layer, static_cast<const char*>(q_dec) + off,
-                             static_cast<char*>(out_dec) + off);
+  // Decode of all layers: split(0); then one launch per layer l >= 1 that merges layer l-1 and
+  // splits layer l into the other partial buffer; finally merge(last). One launch per layer.
+  if (n_dec > 0 && st == CS_OK) {
+    const cs::PoolGeom g = p->geom();
+    const int nl = p->desc.n_layers;
+    const size_t per_layer = static_cast<size_t>(n_dec) * row_bytes;
+    float* buf[2] = {p->partials(), p->partials2()};
+    st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
+      return cs::launch_decode_split(g, 0, dw.convs, dw.n_convs, dw.n_items, dw.split, q_dec, buf[0],
+                                     p->stream);
+    });
+    for (int32_t layer = 1; layer < nl && st == CS_OK; ++layer) {
+      st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode merge+split launch", [&] {
+        return cs::launch_decode_merge_split(
+            g, layer, dw.convs, dw.n_convs, dw.n_items, dw.split,
+            static_cast<const char*>(q_dec) + layer * per_layer, buf[layer % 2], buf[(layer - 1) % 2],
+            static_cast<char*>(out_dec) + (layer - 1) * per_layer, p->stream);
+      });
+    }
+    if (st == CS_OK)
+      st = timed_launch(p, CS_PROF_DECODE_MERGE, "decode merge launch", [&] {
+        return cs::launch_decode_merge(g, dw.convs, dw.n_convs, buf[(nl - 1) % 2],
+                                       static_cast<char*>(out_dec) + (nl - 1) * per_layer, p->stream);
+      });
   }
   if (fork) {  // join even after a failed launch, so later work never overtakes the side stream
     CS_HIP(hipEventRecord(p->join_ev, p->side), "hipEventRecord");

@@ -64,11 +64,11 @@ __device__ __forceinline__ int find_conv(const __attribute__((address_space(4)))
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
+__device__ __forceinline__ void split_body(const DecodeArgs& a, const int block) {
   constexpr int KS = D / 32;  // k-steps of the QK^T contraction
   constexpr int DT = D / 16;  // 16-dim tiles of the output
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int work = blockIdx.x * 4 + wave;  // = item * n_kv_heads + kv head
+  const int work = block * 4 + wave;  // = item * n_kv_heads + kv head
   if (work >= a.n_items * a.n_kv_heads) return;
   const int item = work / a.n_kv_heads, g = work % a.n_kv_heads;
   const auto* convs = as_const(a.convs);
@@ -203,14 +203,13 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
 // (D/4) takes splits sg, sg + SG, ...; dim group = 4 consecutive dims, one 16-byte load); then the
 // split groups added in order 0 .. SG-1.
 template <int D>
-__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
+__device__ __forceinline__ void merge_body(const DecodeArgs& a, const int b, const int h) {
   constexpr int DV = D / 4;          // dim groups (4 dims each)
   constexpr int SG = 256 / DV;       // split groups
   constexpr int R = partial_floats(D);
   __shared__ float red_o[SG][D];
   __shared__ float red_l[SG];
   __shared__ float wave_max[4];
-  const int b = blockIdx.x, h = blockIdx.y;
   const int g = h / a.group, c = h % a.group;
   const DecodeConvDesc cd = load_desc(as_const(a.convs) + b);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -254,6 +253,29 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) { split_body<D>(a, blockIdx.x); }
+
+template <int D>
+__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
+  merge_body<D>(a, blockIdx.x, blockIdx.y);
+}
+
+// The merge of one layer and the split of the next in one launch (a multi-layer step): the first
+// n_conv * n_q_heads workgroups merge layer l's partials (buffer am.partials), the others run layer
+// l+1's split into the other partial buffer. Saves one launch and its gap per layer.
+template <int D>
+__global__ __launch_bounds__(256) void decode_merge_split_kernel(DecodeArgs am, DecodeArgs as) {
+  const int n_merge = am.n_convs * am.n_kv_heads * am.group;
+  const int blk = blockIdx.x;
+  if (blk < n_merge) {
+    const int nqh = am.n_kv_heads * am.group;
+    merge_body<D>(am, blk / nqh, blk % nqh);
+  } else {
+    split_body<D>(as, blk - n_merge);
+  }
+}
+
 static DecodeArgs make_args(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs, int n_convs,
                             int n_items, int split_tokens, const void* q, void* out,
                             const float* partials) {
@@ -284,6 +306,21 @@ hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDes
   const int blocks = (n_items * g.n_kv_heads + 3) / 4;
   if (g.head_dim == 128) decode_split_kernel<128><<<blocks, 256, 0, stream>>>(a);
   else if (g.head_dim == 64) decode_split_kernel<64><<<blocks, 256, 0, stream>>>(a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const DecodeConvDesc* d_convs,
+                                     int n_convs, int n_items, int split_tokens, const void* q,
+                                     float* split_partials, const float* merge_partials,
+                                     void* merge_out, hipStream_t stream) {
+  if (n_convs == 0) return hipSuccess;
+  const DecodeArgs as = make_args(g, split_layer, d_convs, n_convs, n_items, split_tokens, q, nullptr,
+                                  split_partials);
+  const DecodeArgs am = make_args(g, 0, d_convs, n_convs, 0, 0, nullptr, merge_out, merge_partials);
+  const int blocks = n_convs * g.n_q_heads + (n_items * g.n_kv_heads + 3) / 4;
+  if (g.head_dim == 128) decode_merge_split_kernel<128><<<blocks, 256, 0, stream>>>(am, as);
+  else if (g.head_dim == 64) decode_merge_split_kernel<64><<<blocks, 256, 0, stream>>>(am, as);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -40,6 +40,12 @@ hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDes
                                float* partials, hipStream_t stream);
 hipError_t launch_decode_merge(const PoolGeom& g, const DecodeConvDesc* d_convs, int n_convs,
                                const float* partials, void* out, hipStream_t stream);
+// Merge of layer l (merge_partials -> merge_out) and split of layer split_layer (-> split_partials,
+// a different buffer) in one launch; the same conversations and plan for both.
+hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const DecodeConvDesc* d_convs,
+                                     int n_convs, int n_items, int split_tokens, const void* q,
+                                     float* split_partials, const float* merge_partials,
+                                     void* merge_out, hipStream_t stream);
 
 // Query tokens per extend/prefill work tile for this head size and GQA group (the host plan must
 // match).
