@@ -180,12 +180,21 @@ cs_status cs_attn_decode_batch(cs_pool* pool, int32_t n_convs, const cs_conv* co
  * present, the extend launches run on a second stream owned by the pool, forked from `stream`
  * after the append and joined back into it before the call returns: work enqueued on `stream`
  * afterwards (and a synchronisation of `stream`) sees every output of the step.
- * Errors: as cs_kv_append_batch, cs_attn_extend and cs_attn_decode_batch.
+ * flags = 0: every layer's queries are inputs of the call, so no layer waits for another; the
+ *   extend work of all layers overlaps the decode work of all layers, and the decode merge of
+ *   layer l-1 shares one launch with the decode split of layer l (two partial buffers alternate).
+ * flags = CS_MIXED_LAYER_ORDERED: the order of a model forward pass, where layer l+1's queries
+ *   depend on layer l's output: layer l's extend and decode overlap each other, and layer l+1
+ *   starts only when both are complete.
+ * Outputs are bitwise the same either way (and the same as the separate calls).
+ * Errors: as cs_kv_append_batch, cs_attn_extend and cs_attn_decode_batch; CS_EINVAL for unknown
+ * flags.
  */
+enum { CS_MIXED_LAYER_ORDERED = 1 };
 cs_status cs_mixed_step(cs_pool* pool, int32_t n_ext, const cs_conv* ext_convs,
                         const int32_t* ext_lens, int32_t n_dec, const cs_conv* dec_convs,
                         const void* k, const void* v, const void* q_ext, void* out_ext,
-                        const void* q_dec, void* out_dec, cs_stream stream);
+                        const void* q_dec, void* out_dec, uint32_t flags, cs_stream stream);
 
 /* Wire size of a conversation's KV: n_layers * ceil(len/16) * n_kv_heads * 64 * head_dim bytes. */
 cs_status cs_kv_pack_size(const cs_pool* pool, cs_conv conv, size_t* bytes);
@@ -212,8 +221,11 @@ cs_status cs_kv_unpack(cs_pool* pool, const void* src, size_t src_bytes, int64_t
 /*
  * Instrumentation (per-kernel timing; not part of the attention path). Between cs_profile_start
  * and cs_profile_stop every kernel the pool launches is bracketed by two HIP timing events on its
- * stream. cs_profile_stop waits for those events, writes the summed milliseconds and the launch
- * count per kernel kind into ms[CS_PROF_KINDS] and launches[CS_PROF_KINDS], and disables timing.
+ * stream, except in cs_mixed_step, where one pair of events brackets the extend launches of all
+ * layers and one pair the decode launches of all layers but the final merge (their time then
+ * includes the gaps between those launches). cs_profile_stop waits for the events, writes the
+ * summed milliseconds and the launch count per kernel kind into ms[CS_PROF_KINDS] and
+ * launches[CS_PROF_KINDS], and disables timing.
  * Errors: CS_EINVAL (null), CS_EHIP.
  */
 enum {

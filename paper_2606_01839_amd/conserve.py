@@ -16,6 +16,7 @@ import torch
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libconserve_attn.so")
 
 CS_OK, CS_EINVAL, CS_ENOMEM, CS_ENOENT, CS_ESTATE, CS_ERANGE, CS_EHIP, CS_EBUSY = 0, -1, -2, -3, -4, -5, -6, -7
+CS_MIXED_LAYER_ORDERED = 1   # cs_mixed_step flag: layer l+1 starts after layer l
 STATUS_NAMES = {CS_EINVAL: "CS_EINVAL", CS_ENOMEM: "CS_ENOMEM", CS_ENOENT: "CS_ENOENT",
                 CS_ESTATE: "CS_ESTATE", CS_ERANGE: "CS_ERANGE", CS_EHIP: "CS_EHIP",
                 CS_EBUSY: "CS_EBUSY"}
@@ -83,7 +84,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "cs_attn_prefill_turn1": (I32, [P, I32, PI32, PI32, I32, VP, VP, VP]),
         "cs_attn_extend": (I32, [P, I32, PI32, PI32, I32, VP, VP, VP]),
         "cs_attn_decode_batch": (I32, [P, I32, PI32, I32, VP, VP, VP]),
-        "cs_mixed_step": (I32, [P, I32, PI32, PI32, I32, PI32, VP, VP, VP, VP, VP, VP, VP]),
+        "cs_mixed_step": (I32, [P, I32, PI32, PI32, I32, PI32, VP, VP, VP, VP, VP, VP, ctypes.c_uint32, VP]),
         "cs_kv_pack_size": (I32, [P, I32, ctypes.POINTER(SZ)]),
         "cs_kv_pack": (I32, [P, I32, VP, SZ, VP]),
         "cs_kv_unpack": (I32, [P, VP, SZ, I64, PI32, VP]),
@@ -282,9 +283,11 @@ class KVPool:
         return out
 
     def mixed_step(self, ext_convs, ext_lens, dec_convs, k, v, q_ext=None, q_dec=None,
-                   out_ext=None, out_dec=None):
+                   out_ext=None, out_dec=None, layer_ordered=False):
         """One decoder step: extend chunks + one decoded token per decoding conversation, appended
-        for every layer, then attention of every layer. Returns (out_ext, out_dec)."""
+        for every layer, then attention of every layer. With layer_ordered, layer l+1's attention
+        starts only after layer l's (extend and decode of one layer still overlap), as in a model
+        forward pass. Returns (out_ext, out_dec)."""
         ea, ep = _i32_array(ext_convs)
         la, lp = _i32_array(ext_lens)
         da, dp = _i32_array(dec_convs)
@@ -306,8 +309,9 @@ class KVPool:
             if out_dec is None:
                 out_dec = torch.empty(dshape, dtype=torch.bfloat16, device=self.device)
             od = self._dev(out_dec, "out_dec", dshape)
+        flags = CS_MIXED_LAYER_ORDERED if layer_ordered else 0
         _check(self.lib.cs_mixed_step(self._handle, ea.size, ep, lp, nd, dp, kp, vp, qe, oe, qd, od,
-                                      _stream_handle(self.device)))
+                                      flags, _stream_handle(self.device)))
         return out_ext, out_dec
 
     # -- instrumentation -----------------------------------------------------------------------

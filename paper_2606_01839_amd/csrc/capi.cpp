@@ -105,8 +105,14 @@ struct cs_pool {
   struct ProfEvent {
     hipEvent_t start, stop;
     int kind;
+    int launches;
   };
   bool prof_on = false;
+  // an open span: one pair of events brackets a run of launches of one kind on one stream
+  bool span_open = false;
+  hipEvent_t span_start = nullptr;
+  hipStream_t span_stream = nullptr;
+  int span_kind = 0, span_launches = 0;
   std::vector<hipEvent_t> ev_free;
   std::vector<ProfEvent> prof_events;
 
@@ -188,9 +194,15 @@ hipError_t take_event(cs_pool* p, hipEvent_t* e) {
   return hipEventCreate(e);
 }
 
-// Launch a kernel on stream `s`; while profiling, bracket it with timing events on that stream.
+// Launch a kernel on stream `s`; while profiling, bracket it with timing events on that stream
+// (inside an open span the span's events cover it and it only counts as one more launch).
 template <typename F>
 cs_status timed_launch_on(cs_pool* p, hipStream_t s, int kind, const char* what, F&& launch) {
+  if (p->prof_on && p->span_open) {
+    CS_HIP(launch(), what);
+    ++p->span_launches;
+    return CS_OK;
+  }
   hipEvent_t a = nullptr, b = nullptr;
   if (p->prof_on) {
     CS_HIP(take_event(p, &a), "hipEventCreate");
@@ -200,8 +212,46 @@ cs_status timed_launch_on(cs_pool* p, hipStream_t s, int kind, const char* what,
   CS_HIP(launch(), what);
   if (p->prof_on) {
     CS_HIP(hipEventRecord(b, s), "hipEventRecord");
-    p->prof_events.push_back({a, b, kind});
+    p->prof_events.push_back({a, b, kind, 1});
   }
+  return CS_OK;
+}
+
+// Open a timing span of `kind` on stream `s` (no-op while profiling is off). A run of launches
+// then records two events in all instead of two per launch, which keeps the instrumentation's own
+// cost out of multi-layer steps; the span's time includes the short gaps between its launches.
+cs_status span_begin(cs_pool* p, hipStream_t s, int kind) {
+  if (!p->prof_on) return CS_OK;
+  hipEvent_t a = nullptr;
+  CS_HIP(take_event(p, &a), "hipEventCreate");
+  const hipError_t e = hipEventRecord(a, s);
+  if (e != hipSuccess) {
+    p->ev_free.push_back(a);
+    return hip_fail(e, "hipEventRecord");
+  }
+  p->span_start = a;
+  p->span_open = true;
+  p->span_stream = s;
+  p->span_kind = kind;
+  p->span_launches = 0;
+  return CS_OK;
+}
+
+// Close the open span (no-op if none is open); called on error paths too.
+cs_status span_end(cs_pool* p) {
+  if (!p->span_open) return CS_OK;
+  p->span_open = false;
+  hipEvent_t b = nullptr;
+  hipError_t e = take_event(p, &b);
+  if (e == hipSuccess) {
+    e = hipEventRecord(b, p->span_stream);
+    if (e != hipSuccess) p->ev_free.push_back(b);
+  }
+  if (e != hipSuccess) {
+    p->ev_free.push_back(p->span_start);
+    return hip_fail(e, "hipEventRecord");
+  }
+  p->prof_events.push_back({p->span_start, b, p->span_kind, p->span_launches});
   return CS_OK;
 }
 
@@ -670,9 +720,10 @@ cs_status cs_kv_unpack(cs_pool* p, const void* src, size_t src_bytes, int64_t n_
 cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, const int32_t* ext_lens,
                         int32_t n_dec, const cs_conv* dec_convs, const void* k, const void* v,
                         const void* q_ext, void* out_ext, const void* q_dec, void* out_dec,
-                        cs_stream stream) {
+                        uint32_t flags, cs_stream stream) {
   if (!p) return fail(CS_EINVAL, "null pool");
   if (n_ext < 0 || n_dec < 0) return fail(CS_EINVAL, "negative batch size");
+  if (flags & ~static_cast<uint32_t>(CS_MIXED_LAYER_ORDERED)) return fail(CS_EINVAL, "unknown flags");
   if ((n_ext > 0 && (!ext_convs || !ext_lens)) || (n_dec > 0 && !dec_convs))
     return fail(CS_EINVAL, "null conversation or length array");
   std::vector<cs_conv> all;
@@ -715,52 +766,78 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
   if (n_ext > 0 && (st = upload_extend(p, e_slots, e_lens, e_q, &ew)) != CS_OK) return st;
   if (n_dec > 0 && (st = upload_decode(p, d_slots, d_lens, &dw)) != CS_OK) return st;
   const size_t row_bytes = static_cast<size_t>(p->desc.n_q_heads) * p->desc.head_dim * 2;
-  // Extend chunks and decode tokens of the step are independent once their K/V is appended: with
-  // both present the extend launches (all layers) go to a second stream that forks after the
-  // uploads and joins before the call returns, so the matrix-core-bound extend work overlaps the
-  // HBM-bound decode work.
+  const int nl = p->desc.n_layers;
+  const size_t ext_layer_bytes = static_cast<size_t>(ext_rows) * row_bytes;
+  const size_t dec_layer_bytes = static_cast<size_t>(n_dec) * row_bytes;
+  auto q_e = [&](int l) { return static_cast<const char*>(q_ext) + l * ext_layer_bytes; };
+  auto o_e = [&](int l) { return static_cast<char*>(out_ext) + l * ext_layer_bytes; };
+  auto q_d = [&](int l) { return static_cast<const char*>(q_dec) + l * dec_layer_bytes; };
+  auto o_d = [&](int l) { return static_cast<char*>(out_dec) + l * dec_layer_bytes; };
+  // Extend chunks and decode tokens are independent once their K/V is appended: with both present
+  // the extend launches go to a second stream (forked from `stream`, joined back before the call
+  // returns), so the matrix-core-bound extend work overlaps the HBM-bound decode work.
   const bool fork = n_ext > 0 && n_dec > 0;
   hipStream_t ext_stream = p->stream;
-  if (fork) {
-    if ((st = ensure_side(p)) != CS_OK) return st;
+  if (fork && (st = ensure_side(p)) != CS_OK) return st;
+  if (fork) ext_stream = p->side;
+  auto fork_side = [&]() -> cs_status {
     CS_HIP(hipEventRecord(p->fork_ev, p->stream), "hipEventRecord");
     CS_HIP(hipStreamWaitEvent(p->side, p->fork_ev, 0), "hipStreamWaitEvent");
-    ext_stream = p->side;
+    return CS_OK;
+  };
+  auto join_side = [&]() -> cs_status {
+    CS_HIP(hipEventRecord(p->join_ev, p->side), "hipEventRecord");
+    CS_HIP(hipStreamWaitEvent(p->stream, p->join_ev, 0), "hipStreamWaitEvent");
+    return CS_OK;
+  };
+  if (flags & CS_MIXED_LAYER_ORDERED) {
+    // As in a model forward pass: layer l's extend and decode overlap each other, and layer l+1
+    // starts only once both are complete.
+    for (int layer = 0; layer < nl && st == CS_OK; ++layer) {
+      if (fork && (st = fork_side()) != CS_OK) return st;
+      if (n_ext > 0) st = launch_extend_layer(p, ew, layer, q_e(layer), o_e(layer), ext_stream);
+      if (n_dec > 0 && st == CS_OK) st = launch_decode_layer(p, dw, layer, q_d(layer), o_d(layer));
+      if (fork) {  // join even after a failed launch, so later work never overtakes the side stream
+        const cs_status sj = join_side();
+        if (st == CS_OK) st = sj;
+      }
+    }
+    return st;
   }
-  for (int32_t layer = 0; layer < p->desc.n_layers && n_ext > 0; ++layer) {
-    const size_t off = static_cast<size_t>(layer) * static_cast<size_t>(ext_rows) * row_bytes;
-    if ((st = launch_extend_layer(p, ew, layer, static_cast<const char*>(q_ext) + off,
-                                  static_cast<char*>(out_ext) + off, ext_stream)) != CS_OK)
-      break;
-  }
+  // Every layer's queries are inputs of this call, so no layer waits for another: the extend
+  // launches of all layers run on the side stream while the main stream decodes all layers.
+  if (fork && (st = fork_side()) != CS_OK) return st;
+  if (n_ext > 0) st = span_begin(p, ext_stream, CS_PROF_ATTN_FWD);
+  for (int layer = 0; layer < nl && n_ext > 0 && st == CS_OK; ++layer)
+    st = launch_extend_layer(p, ew, layer, q_e(layer), o_e(layer), ext_stream);
+  if (const cs_status se = span_end(p); st == CS_OK) st = se;
   // Decode of all layers: split(0); then one launch per layer l >= 1 that merges layer l-1 and
   // splits layer l into the other partial buffer; finally merge(last). One launch per layer.
   if (n_dec > 0 && st == CS_OK) {
     const cs::PoolGeom g = p->geom();
-    const int nl = p->desc.n_layers;
-    const size_t per_layer = static_cast<size_t>(n_dec) * row_bytes;
     float* buf[2] = {p->partials(), p->partials2()};
-    st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
-      return cs::launch_decode_split(g, 0, dw.convs, dw.n_convs, dw.n_items, dw.split, q_dec, buf[0],
+    st = span_begin(p, p->stream, CS_PROF_DECODE_SPLIT);
+    if (st == CS_OK) st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
+      return cs::launch_decode_split(g, 0, dw.convs, dw.n_convs, dw.n_items, dw.split, q_d(0), buf[0],
                                      p->stream);
     });
-    for (int32_t layer = 1; layer < nl && st == CS_OK; ++layer) {
+    for (int layer = 1; layer < nl && st == CS_OK; ++layer) {
       st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode merge+split launch", [&] {
-        return cs::launch_decode_merge_split(
-            g, layer, dw.convs, dw.n_convs, dw.n_items, dw.split,
-            static_cast<const char*>(q_dec) + layer * per_layer, buf[layer % 2], buf[(layer - 1) % 2],
-            static_cast<char*>(out_dec) + (layer - 1) * per_layer, p->stream);
+        return cs::launch_decode_merge_split(g, layer, dw.convs, dw.n_convs, dw.n_items, dw.split,
+                                             q_d(layer), buf[layer % 2], buf[(layer - 1) % 2],
+                                             o_d(layer - 1), p->stream);
       });
     }
+    if (const cs_status se = span_end(p); st == CS_OK) st = se;
     if (st == CS_OK)
       st = timed_launch(p, CS_PROF_DECODE_MERGE, "decode merge launch", [&] {
-        return cs::launch_decode_merge(g, dw.convs, dw.n_convs, buf[(nl - 1) % 2],
-                                       static_cast<char*>(out_dec) + (nl - 1) * per_layer, p->stream);
+        return cs::launch_decode_merge(g, dw.convs, dw.n_convs, buf[(nl - 1) % 2], o_d(nl - 1),
+                                       p->stream);
       });
   }
   if (fork) {  // join even after a failed launch, so later work never overtakes the side stream
-    CS_HIP(hipEventRecord(p->join_ev, p->side), "hipEventRecord");
-    CS_HIP(hipStreamWaitEvent(p->stream, p->join_ev, 0), "hipStreamWaitEvent");
+    const cs_status sj = join_side();
+    if (st == CS_OK) st = sj;
   }
   return st;
 }
@@ -788,7 +865,7 @@ cs_status cs_profile_stop(cs_pool* p, double* ms, int64_t* launches) {
     float t = 0.f;
     CS_HIP(hipEventElapsedTime(&t, pe.start, pe.stop), "hipEventElapsedTime");
     ms[pe.kind] += t;
-    launches[pe.kind] += 1;
+    launches[pe.kind] += pe.launches;
     p->ev_free.push_back(pe.start);
     p->ev_free.push_back(pe.stop);
   }

@@ -86,3 +86,63 @@ def test_mixed_step_rejects_overlap_without_changes():
     assert e.value.code == CS_EINVAL
     assert pool.conv_len(a) == 10 and pool.occupancy()[0] == 1
     pool.close()
+
+
+@pytest.mark.parametrize("layer_ordered", [False, True])
+@pytest.mark.parametrize("n_layers", [1, 3, 4])
+def test_mixed_step_bitwise_equals_per_layer_calls(n_layers, layer_ordered):
+    """The mixed step gives bit for bit the outputs of the separate calls (kv_append_batch, then
+    attn_extend and attn_decode_batch layer by layer, on a second pool with the same placement),
+    both with all layers overlapped (one launch per layer that merges layer l-1 and splits layer l,
+    alternating two partial buffers) and in layer order. Decode-only and extend-only steps
+    included; the last layer's decode outputs are checked against the oracle."""
+    from paper_2606_01839_amd import KVPool
+    mk = lambda: KVPool(n_layers, HQ, HKV, D, n_pages=900, max_convs=8, max_pages_per_conv=256,
+                        placement_seed=77)
+    pa, pb = mk(), mk()
+    lens0 = [1200, 5, 417, 2049, 96, 800]
+    ha, hb, lens = [], [], list(lens0)
+
+    def kv_rows(items):
+        ks = [torch.stack([_kv(c, l, s, n)[0] for l in range(n_layers)]) for c, s, n in items]
+        vs = [torch.stack([_kv(c, l, s, n)[1] for l in range(n_layers)]) for c, s, n in items]
+        return torch.cat(ks, 1).contiguous().cuda(), torch.cat(vs, 1).contiguous().cuda()
+
+    for c, L in enumerate(lens0):
+        k, v = kv_rows([(c, 0, L)])
+        for pool, hs in ((pa, ha), (pb, hb)):
+            h = pool.conv_create()
+            pool.kv_append(h, k, v)
+            hs.append(h)
+    plans = [([0, 4], [300, 33], [1, 2, 3, 5]), ([], [], [0, 1, 2, 3, 4, 5]), ([1, 3], [64, 2], [])]
+    for ext, ext_n, dec in plans:
+        items = [(c, lens[c], n) for c, n in zip(ext, ext_n)] + [(c, lens[c], 1) for c in dec]
+        k, v = kv_rows(items)
+        qe = (torch.stack([torch.cat([_q(c, l, lens[c], n) for c, n in zip(ext, ext_n)])
+                           for l in range(n_layers)]).contiguous().cuda() if ext else None)
+        qd = (torch.stack([torch.cat([_q(c, l, lens[c], 1) for c in dec])
+                           for l in range(n_layers)]).contiguous().cuda() if dec else None)
+        oe, od = pa.mixed_step([ha[c] for c in ext], ext_n, [ha[c] for c in dec], k, v, qe, qd,
+                              layer_ordered=layer_ordered)
+        pb.kv_append_batch([hb[c] for c, _, _ in items], [n for _, _, n in items], k, v)
+        for layer in range(n_layers):
+            if ext:
+                ref_e = pb.attn_extend([hb[c] for c in ext], ext_n, layer, qe[layer])
+                assert torch.equal(oe[layer], ref_e), f"extend layer {layer} of plan {ext}/{dec}"
+            if dec:
+                ref_d = pb.attn_decode_batch([hb[c] for c in dec], layer, qd[layer])
+                assert torch.equal(od[layer], ref_d), f"decode layer {layer} of plan {ext}/{dec}"
+        torch.cuda.synchronize()
+        for c, s, n in items:
+            lens[c] = s + n
+        if dec:
+            layer = n_layers - 1
+            for i, c in enumerate(dec):
+                kk, vv = _kv(c, layer, 0, lens[c])
+                ref = attend_last(sv.bf16_to_f64(qd[layer, i:i + 1]), sv.bf16_to_f64(kk), sv.bf16_to_f64(vv))
+                assert_close(od[layer, i:i + 1], ref, f"decode conv {c} layer {layer}")
+    for c in range(len(lens0)):
+        assert pa.conv_len(ha[c]) == pb.conv_len(hb[c]) == lens[c]
+    assert pa.occupancy() == pb.occupancy()
+    pa.close()
+    pb.close()

@@ -99,6 +99,15 @@ def test_conversation_lifecycle_and_errors():
         p.kv_unpack(torch.zeros(100, dtype=torch.uint8), 3)
     assert e.value.code in (CS_EINVAL, CS_ENOMEM)
     assert p.kv_pack_size(a) == 0
+    # unknown mixed-step flags are rejected before anything is appended
+    from paper_2606_01839_amd.conserve import _i32_array
+    ca, cp = _i32_array([a])
+    na, npp = _i32_array([1])
+    kk = torch.zeros(1, 1, 2, 64, dtype=torch.bfloat16)
+    qq = torch.zeros(1, 1, 4, 64, dtype=torch.bfloat16)
+    rc = p.lib.cs_mixed_step(p._handle, 1, cp, npp, 0, None, kk.data_ptr(), kk.data_ptr(),
+                             qq.data_ptr(), qq.data_ptr(), None, None, 2, None)
+    assert rc == CS_EINVAL and p.conv_len(a) == 0
     p.close()
 
 
