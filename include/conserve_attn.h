@@ -72,7 +72,8 @@ typedef struct {
 /*
  * KV pool layout (device, caller-allocated, cs_pool_kv_bytes(desc) bytes, 256-byte aligned):
  *   pool[layer][page][kv_head] = one 4*16*head_dim-byte block:
- *     K[16][head_dim]  token-major rows, then
+ *     K part: head_dim/32 sub-blocks, sub-block s = K[16 tokens][dims 32s .. 32s+31] token-major
+ *             (each sub-block 1 KiB: what one matrix-core operand load of 16 keys reads), then
  *     V^T[head_dim][16] dimension-major (each row holds one dimension of the page's 16 tokens).
  * Token slots >= length in a conversation's last page always hold zeros (append and unpack write
  * them), so a page is never read past the conversation's end with undefined contents.
@@ -202,8 +203,8 @@ cs_status cs_kv_pack_size(const cs_pool* pool, cs_conv conv, size_t* bytes);
 /*
  * Gather a conversation's pages in logical order into a contiguous wire buffer (the sending half
  * of the one-time turn-1 KV transfer, Section 4 and Section 3.1 "KV cache transfer").
- * Wire layout: [layer][logical page][kv_head] blocks in the pool's block format (K[16][d] then
- * V^T[d][16]); token slots >= length are written as zeros. dst: device, dst_bytes must equal
+ * Wire layout: [layer][logical page][kv_head] blocks in the pool's block format (K part in
+ * 32-dim token-major sub-blocks, then V^T[d][16]); token slots >= length are written as zeros. dst: device, dst_bytes must equal
  * cs_kv_pack_size. Errors: CS_ENOENT, CS_EINVAL, CS_EHIP.
  */
 cs_status cs_kv_pack(const cs_pool* pool, cs_conv conv, void* dst, size_t dst_bytes,

@@ -10,11 +10,12 @@ What it follows
 The paper does not fix a wire format (its transfer goes through a KV-cache manager whose layout it
 does not state). The format adopted here is header-free, logical page order, 16 tokens per page:
 
-    wire = [layer][logical page][kv head] blocks, each block = K[16][d] followed by V^T[d][16]
+    wire = [layer][logical page][kv head] blocks, each block = K part followed by V^T[d][16]
 
-in bf16 (stored as uint16 bit patterns), token slots >= L of the last page zero. K rows are
-token-major, V is stored dimension-major (transposed) inside each block. Size in bytes:
-n_layers * ceil(L/16) * Hkv * 2 * 16 * d * 2.
+in bf16 (stored as uint16 bit patterns), token slots >= L of the last page zero. The K part is
+d/w sub-blocks of w = min(d, 32) dims, sub-block s = K[16 tokens][dims w*s .. w*s + w - 1]
+token-major (for d <= 32 that is simply K[16][d]); V is stored dimension-major (transposed). Size
+in bytes: n_layers * ceil(L/16) * Hkv * 2 * 16 * d * 2.
 
 Everything here is byte movement: results are compared bit for bit.
 """
@@ -48,9 +49,17 @@ def wire_bytes(n_layers: int, length: int, n_kv_heads: int, head_dim: int) -> in
     return n_layers * pages * n_kv_heads * 2 * PAGE * head_dim * 2
 
 
+def k_sub_width(d: int) -> int:
+    """Width w of the K sub-blocks of a block (d must be a multiple of it)."""
+    w = min(d, 32)
+    assert d % w == 0, "head_dim must be <= 32 or a multiple of 32"
+    return w
+
+
 def serialize(k: np.ndarray, v: np.ndarray) -> np.ndarray:
     """k, v: [n_layers][L][Hkv][d] uint16 -> wire buffer as a flat uint16 array."""
     n_layers, L, hkv, d = k.shape
+    w = k_sub_width(d)
     pages = (L + PAGE - 1) // PAGE
     out = np.zeros((n_layers, pages, hkv, 2, PAGE * d), dtype=np.uint16)
     for layer in range(n_layers):
@@ -61,7 +70,8 @@ def serialize(k: np.ndarray, v: np.ndarray) -> np.ndarray:
                 vb = np.zeros((PAGE, d), dtype=np.uint16)
                 kb[: t1 - t0] = k[layer, t0:t1, h]
                 vb[: t1 - t0] = v[layer, t0:t1, h]
-                out[layer, p, h, 0] = kb.reshape(-1)          # token-major K rows
+                # K sub-blocks: [d/w][16 tokens][w dims]
+                out[layer, p, h, 0] = kb.reshape(PAGE, d // w, w).transpose(1, 0, 2).reshape(-1)
                 out[layer, p, h, 1] = vb.T.reshape(-1)        # dimension-major V columns
     return out.reshape(-1)
 
@@ -69,14 +79,16 @@ def serialize(k: np.ndarray, v: np.ndarray) -> np.ndarray:
 def deserialize(wire: np.ndarray, n_layers: int, length: int, n_kv_heads: int, head_dim: int):
     """Inverse of ``serialize``: wire (flat uint16) -> (k, v) [n_layers][L][Hkv][d] uint16."""
     pages = (length + PAGE - 1) // PAGE
-    w = np.asarray(wire, dtype=np.uint16).reshape(n_layers, pages, n_kv_heads, 2, PAGE, head_dim)
+    sw = k_sub_width(head_dim)
+    w = np.asarray(wire, dtype=np.uint16).reshape(n_layers, pages, n_kv_heads, 2, PAGE * head_dim)
     k = np.zeros((n_layers, length, n_kv_heads, head_dim), dtype=np.uint16)
     v = np.zeros_like(k)
     for layer in range(n_layers):
         for p in range(pages):
             t0, t1 = p * PAGE, min(length, (p + 1) * PAGE)
             for h in range(n_kv_heads):
-                k[layer, t0:t1, h] = w[layer, p, h, 0][: t1 - t0]
+                kb = w[layer, p, h, 0].reshape(head_dim // sw, PAGE, sw).transpose(1, 0, 2)
+                k[layer, t0:t1, h] = kb.reshape(PAGE, head_dim)[: t1 - t0]
                 vt = w[layer, p, h, 1].reshape(head_dim, PAGE)
                 v[layer, t0:t1, h] = vt.T[: t1 - t0]
     return k, v

@@ -186,7 +186,8 @@ class KVPool:
         return 2 * PAGE_TOKENS * self.head_dim * 2
 
     def kv_view(self) -> torch.Tensor:
-        """The pool as [n_layers][n_pages][n_kv_heads][2*16*head_dim] bf16 bits (int16 view)."""
+        """The pool as [n_layers][n_pages][n_kv_heads][2*16*head_dim] bf16 bits (int16 view); each
+        block is the K part (head_dim/32 sub-blocks [16 tokens][32 dims]) then V^T[head_dim][16]."""
         return self.kv.view(torch.int16).view(self.n_layers, self.desc.n_pages, self.n_kv_heads,
                                               2 * PAGE_TOKENS * self.head_dim)
 

@@ -140,7 +140,7 @@ void attn_fwd_kernel(ExtendArgs a) {
     // LDS row 8a + 4h + b holds key 8h + 4a + b (bits 2 and 3 swapped): the S^T accumulator
     // of lane half h then holds keys 8h .. 8h+7 of each 16-key step, the order of V^T in LDS.
     const int key = ((quarter & 1) << 3 | (quarter >> 1) << 2) + lane / 16;
-    koff[i] = static_cast<uint32_t>(key * (2 * D) + chunk * 16);
+    koff[i] = static_cast<uint32_t>(k_elem(key, chunk) * 2);
     const int dim = 32 * quarter + lane / 2;
     const int hv = (lane & 1) ^ ((dim >> 2) & 1) ^ ((dim >> 3) & 1);
     voff[i] = static_cast<uint32_t>(2 * kPageTokens * D + dim * 32 + hv * 16);
@@ -379,7 +379,7 @@ void attn_fwd_staged_kernel(ExtendArgs a) {
       const int lp = min(__builtin_amdgcn_readfirstlane(4 * j + i / (2 * D)), n_pg - 1);
       const int w = i % (2 * D);
       const uint16_t* blk = a.pool + layer_base + static_cast<size_t>(ptc[lp]) * page_stride;
-      kreg[u] = ld16(blk + w * 8);                          // K: row w/(D/8), chunk w%(D/8)
+      kreg[u] = ld16(blk + w * 8);                          // K: sub-block w/64, key (w%64)/4
       vreg[u] = ld16(blk + kPageTokens * D + w * 8);        // V^T: dim w/2, keys 8*(w%2)..+8
     }
   };
@@ -392,7 +392,8 @@ void attn_fwd_staged_kernel(ExtendArgs a) {
     for (int u = 0; u < PER; ++u) {
       const int i = tid + u * NT;
       const int p = i / (2 * D), w = i % (2 * D);
-      const int row = kPageTokens * p + w / (D / 8), col8 = (w % (D / 8)) * 8;
+      // K chunk w of the block: sub-block w / 64, key (w % 64) / 4, dims 32 (w / 64) + 8 (w % 4)
+      const int row = kPageTokens * p + (w & 63) / 4, col8 = ((w >> 6) * 4 + (w & 3)) * 8;
       uint4 kx = kreg[u], vx = vreg[u];
       if (tail) {
         if (4 * j + p >= n_pg) kx = make_uint4(0, 0, 0, 0);

@@ -7,7 +7,8 @@
 //                                                     B = Q, 8 consecutive dims per lane)
 //   O^T[dim][head] += V^T[dim][key] . P^T[key][head]  (A = V^T rows from the page,
 //                                                     B = P from the S^T accumulator registers)
-// so K and V^T are used in the layout they are stored in (coalesced 16/8-byte loads, no LDS).
+// so K and V^T are used in the layout they are stored in (no LDS): each K operand load reads one
+// 1 KiB sub-block of a page, each V^T load 512 consecutive bytes.
 // The softmax is online in fp32 (exp2 with log2(e)/sqrt(d) folded into the score scale); the
 // per-item partial (o, m, l) goes to a workspace and a second kernel merges the splits of each
 // (conversation, query head) in a fixed order. No atomics: bitwise deterministic, and split
@@ -102,9 +103,9 @@ __device__ __forceinline__ void split_body(const DecodeArgs& a, const int block)
   const uint16_t* layer_base = a.pool + static_cast<size_t>(a.layer) * a.n_pages * a.n_kv_heads * head_stride +
                                static_cast<size_t>(g) * head_stride;
   const size_t page_stride = static_cast<size_t>(a.n_kv_heads) * head_stride;
-  // Per-lane byte offsets inside a page block (the same for every page): K row c, dims 8 qd ..;
-  // V^T row c (of a 16-dim tile), keys 4 qd .. 4 qd + 3.
-  const uint32_t koff = static_cast<uint32_t>((c * D + 8 * qd) * 2);
+  // Per-lane byte offsets inside a page block (the same for every page): key c, dims 8 qd ..
+  // (+32 ks: next K sub-block, 1 KiB on); V^T row c (of a 16-dim tile), keys 4 qd .. 4 qd + 3.
+  const uint32_t koff = static_cast<uint32_t>((c * 32 + 8 * qd) * 2);
   const uint32_t voff = static_cast<uint32_t>((kPageTokens * D + c * kPageTokens + 4 * qd) * 2);
 
   for (int j = 0; j < n_pg; j += 2) {
@@ -117,12 +118,12 @@ __device__ __forceinline__ void split_body(const DecodeArgs& a, const int block)
     bf16x8 ka[KS], kb[KS];
     uint2 va[DT], vb[DT];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) ka[ks] = as_bf16x8(ld16_nt(blk_a + koff + 64 * ks));
+    for (int ks = 0; ks < KS; ++ks) ka[ks] = as_bf16x8(ld16_nt(blk_a + koff + 1024 * ks));
 #pragma unroll
     for (int t = 0; t < DT; ++t) va[t] = ld8_nt(blk_a + voff + 16 * kPageTokens * 2 * t);
     if (has_b) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kb[ks] = as_bf16x8(ld16_nt(blk_b + koff + 64 * ks));
+      for (int ks = 0; ks < KS; ++ks) kb[ks] = as_bf16x8(ld16_nt(blk_b + koff + 1024 * ks));
 #pragma unroll
       for (int t = 0; t < DT; ++t) vb[t] = ld8_nt(blk_b + voff + 16 * kPageTokens * 2 * t);
     } else {

@@ -16,7 +16,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-// Pool block of (layer, page, kv head): K[16][D] then V^T[D][16], bf16. Offsets in elements.
+// Pool block of (layer, page, kv head), bf16: the K part, then V^T[D][16] (dimension-major). The
+// K part is D/32 sub-blocks of 32 dims, each K[16 tokens][32 dims] token-major: the 64-byte pieces
+// of one 32-dim range of all 16 keys are 1 KiB of consecutive bytes, which is what one 16-byte-
+// per-lane load of the matrix-core K operand (16 keys x 4 lanes) reads. Offsets in elements.
 template <int D>
 __device__ __forceinline__ size_t block_elem(int layer, int page, int head, int64_t n_pages,
                                              int n_kv_heads) {
@@ -24,6 +27,11 @@ __device__ __forceinline__ size_t block_elem(int layer, int page, int head, int6
               static_cast<size_t>(n_kv_heads) +
           static_cast<size_t>(head)) *
          static_cast<size_t>(2 * kPageTokens * D);
+}
+
+// Element offset inside a block of dims 8 chunk .. 8 chunk + 7 of token t (K part).
+__device__ __forceinline__ int k_elem(int t, int chunk) {
+  return ((chunk >> 2) * kPageTokens + t) * 32 + (chunk & 3) * 8;
 }
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }

@@ -1,14 +1,15 @@
 // KV movement kernels: append new tokens into pages, pack a conversation into the transfer wire
 // format, unpack a wire buffer into freshly placed pages. Pure byte movement (bit-exact); every
-// one is HBM-bound. A pool block (layer, page, kv head) is K[16][D] token-major followed by
-// V^T[D][16] dimension-major; token slots past a conversation's end are kept zero.
+// one is HBM-bound. A pool block (layer, page, kv head) is its K part (D/32 token-major sub-blocks
+// of 32 dims, see k_elem) followed by V^T[D][16] dimension-major; token slots past a
+// conversation's end are kept zero. The wire format of the transfer is the same block format.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
 namespace cs {
 
 // ---------------------------------------------------------------------------------------------
-// Append: one wave per (page chunk, layer, kv head). K rows are copied with 16-byte accesses;
+// Append: one wave per (page chunk, layer, kv head). K pieces are copied with 16-byte accesses;
 // V rows are staged in LDS and written transposed. Slots [t1, 16) of the chunk's page are zeroed.
 // ---------------------------------------------------------------------------------------------
 template <int D>
@@ -41,7 +42,7 @@ __global__ __launch_bounds__(64) void kv_append_kernel(const PageChunk* __restri
       kv = ld16(k_src + src);
       vv = ld16(v_src + src);
     }
-    if (t >= c.t0) st16(blk + t * D + ch * 8, kv);
+    if (t >= c.t0) st16(blk + k_elem(t, ch), kv);
     *reinterpret_cast<uint4*>(&vt[t][ch * 8]) = vv;
   }
   __syncthreads();
@@ -69,8 +70,8 @@ __global__ __launch_bounds__(64) void kv_append_kernel(const PageChunk* __restri
 template <int D>
 __device__ __forceinline__ uint4 mask_tail(uint4 x, int i, int valid) {
   const int e0 = 8 * i;
-  if (e0 < kPageTokens * D) {           // K part: chunk lies in token row e0 / D
-    return (e0 / D) < valid ? x : make_uint4(0, 0, 0, 0);
+  if (e0 < kPageTokens * D) {           // K part: chunk i holds dims of token (i % 64) / 4
+    return ((i & 63) >> 2) < valid ? x : make_uint4(0, 0, 0, 0);
   }
   const int t0 = (e0 - kPageTokens * D) % kPageTokens;  // V^T part: tokens t0 .. t0+7 of one dim
   x.x = mask_bf16x2(x.x, t0 + 0 < valid, t0 + 1 < valid);

@@ -33,7 +33,9 @@ def _gather_pool(pool, conv, n_layers, hkv, d):
     for lp, pg in enumerate(pages):
         t0, t1 = 16 * lp, min(L, 16 * lp + 16)
         b = blocks[:, pg]                                 # [layer][head][2*16*d]
-        kb = b[..., : 16 * d].reshape(n_layers, hkv, 16, d)
+        # K part: d/32 sub-blocks of 32 dims, each [16 tokens][32 dims]
+        kb = b[..., : 16 * d].reshape(n_layers, hkv, d // 32, 16, 32).transpose(0, 1, 3, 2, 4)
+        kb = kb.reshape(n_layers, hkv, 16, d)
         vb = b[..., 16 * d:].reshape(n_layers, hkv, d, 16)
         k[:, t0:t1] = kb[:, :, : t1 - t0].transpose(0, 2, 1, 3)
         v[:, t0:t1] = vb[:, :, :, : t1 - t0].transpose(0, 3, 1, 2)

@@ -186,10 +186,31 @@ def test_wire_hand_written_golden():
     assert np.array_equal(got, wire)
 
 
+def test_wire_hand_written_golden_d64_sub_blocks():
+    lines = [l.split("#")[0].split() for l in open(os.path.join(GOLDEN, "wire_d64_two_tokens.txt"))]
+    lines = [l for l in lines if l]
+    nl, L, hkv, d = [int(x) for x in lines[0][1:]]
+    want = np.zeros(kvwire.wire_bytes(nl, L, hkv, d) // 2, dtype=np.uint16)
+    for l in lines[1:]:
+        assert l[0] == "runs"
+        P, N, V, S, R, PS, VS = (int(x) for x in l[1:])
+        for r in range(R):
+            for i in range(N):
+                want[P + r * PS + i] = V + r * VS + i * S
+    t = np.arange(L)[:, None]
+    j = np.arange(d)[None, :]
+    k = (1000 + 100 * t + j).astype(np.uint16).reshape(nl, L, hkv, d)
+    v = (5000 + 100 * t + j).astype(np.uint16).reshape(nl, L, hkv, d)
+    assert np.array_equal(kvwire.serialize(k, v), want)
+    k2, v2 = kvwire.deserialize(want, nl, L, hkv, d)
+    assert np.array_equal(k2, k) and np.array_equal(v2, v)
+
+
+@pytest.mark.parametrize("d", [8, 64])
 @pytest.mark.parametrize("L", [1, 15, 16, 17, 48, 100])
-def test_wire_round_trip_and_zero_tail(L):
+def test_wire_round_trip_and_zero_tail(L, d):
     rng = np.random.default_rng(L)
-    nl, hkv, d = 2, 3, 8
+    nl, hkv = 2, 3
     k = rng.integers(1, 65536, size=(nl, L, hkv, d), dtype=np.uint16)
     v = rng.integers(1, 65536, size=(nl, L, hkv, d), dtype=np.uint16)
     w = kvwire.serialize(k, v)
@@ -200,7 +221,8 @@ def test_wire_round_trip_and_zero_tail(L):
     pages = (L + 15) // 16
     blk = w.reshape(nl, pages, hkv, 2, 16 * d)
     tail = L - (pages - 1) * 16
-    kl = blk[:, -1, :, 0].reshape(nl, hkv, 16, d)
+    sw = min(d, 32)                                        # K sub-blocks [d/sw][16][sw]
+    kl = blk[:, -1, :, 0].reshape(nl, hkv, d // sw, 16, sw).transpose(0, 1, 3, 2, 4)
     vl = blk[:, -1, :, 1].reshape(nl, hkv, d, 16)
     assert (kl[:, :, tail:] == 0).all() and (vl[:, :, :, tail:] == 0).all()
     # every nonzero input value appears exactly once in the wire (pure movement)
