@@ -9,11 +9,16 @@
 namespace cs {
 
 // ---------------------------------------------------------------------------------------------
-// Append: one wave per (page chunk, layer, kv head). K pieces are copied with 16-byte accesses;
-// V rows are staged in LDS and written transposed. Slots [t1, 16) of the chunk's page are zeroed.
+// Append: one wave per (layer, kv head) and kAppendChunks page chunks, up to 4 kv heads per
+// workgroup. A wave issues the loads of all its chunks before any store (more bytes in flight per
+// wave, half as many waves), copies K pieces with 16-byte accesses, and stages V rows in LDS to
+// write them transposed. Slots [t1, 16) of each chunk's page are zeroed.
 // ---------------------------------------------------------------------------------------------
+constexpr int kAppendChunks = 2;
+
 template <int D>
-__global__ __launch_bounds__(64) void kv_append_kernel(const PageChunk* __restrict__ chunks,
+__global__ __launch_bounds__(256) void kv_append_kernel(const PageChunk* __restrict__ chunks,
+                                                       int n_chunks,
                                                        const uint16_t* __restrict__ k_src,
                                                        const uint16_t* __restrict__ v_src,
                                                        int64_t src_rows, uint16_t* __restrict__ pool,
@@ -22,48 +27,75 @@ __global__ __launch_bounds__(64) void kv_append_kernel(const PageChunk* __restri
                                                        int max_pages) {
   constexpr int kChunksPerRow = D / 8;            // 16-byte chunks per token row
   constexpr int kRowsPerPass = 64 / kChunksPerRow;
-  __shared__ uint16_t vt[kPageTokens][D + 8];
+  constexpr int kPasses = kPageTokens / kRowsPerPass;
+  constexpr int CH = kAppendChunks;
+  __shared__ uint16_t vts[4][CH][kPageTokens][D + 8];
 
-  const PageChunk c = chunks[blockIdx.x];
-  const int layer = blockIdx.y / n_kv_heads;
-  const int head = blockIdx.y % n_kv_heads;
-  const int lane = threadIdx.x;
-  uint16_t* blk = pool + block_elem<D>(layer, c.page, head, n_pages, n_kv_heads);
-
+  const int waves = blockDim.x >> 6, wave = threadIdx.x >> 6;
+  const int groups = n_kv_heads / waves;  // workgroups per (chunk group, layer)
+  const int layer = blockIdx.y / groups;
+  const int head = (blockIdx.y % groups) * waves + wave;
+  const int lane = threadIdx.x & 63;
   const int ch = lane % kChunksPerRow;
+
+  PageChunk c[CH];
+  bool have[CH];
+  uint4 kv[CH][kPasses], vv[CH][kPasses];
 #pragma unroll
-  for (int t = lane / kChunksPerRow; t < kPageTokens; t += kRowsPerPass) {
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (t >= c.t0 && t < c.t1) {
-      const size_t row = static_cast<size_t>(c.src_row) + static_cast<size_t>(t - c.t0);
-      const size_t src =
-          ((static_cast<size_t>(layer) * static_cast<size_t>(src_rows) + row) * n_kv_heads + head) *
-              D + ch * 8;
-      kv = ld16(k_src + src);
-      vv = ld16(v_src + src);
+  for (int i = 0; i < CH; ++i) {
+    const int idx = blockIdx.x * CH + i;
+    have[i] = idx < n_chunks;
+    c[i] = chunks[have[i] ? idx : 0];
+#pragma unroll
+    for (int ps = 0; ps < kPasses; ++ps) {
+      const int t = lane / kChunksPerRow + ps * kRowsPerPass;
+      kv[i][ps] = make_uint4(0, 0, 0, 0);
+      vv[i][ps] = make_uint4(0, 0, 0, 0);
+      if (have[i] && t >= c[i].t0 && t < c[i].t1) {
+        const size_t row = static_cast<size_t>(c[i].src_row) + static_cast<size_t>(t - c[i].t0);
+        const size_t src =
+            ((static_cast<size_t>(layer) * static_cast<size_t>(src_rows) + row) * n_kv_heads + head) *
+                D + ch * 8;
+        kv[i][ps] = ld16(k_src + src);
+        vv[i][ps] = ld16(v_src + src);
+      }
     }
-    if (t >= c.t0) st16(blk + k_elem(t, ch), kv);
-    *reinterpret_cast<uint4*>(&vt[t][ch * 8]) = vv;
+  }
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    if (!have[i]) continue;
+    uint16_t* blk = pool + block_elem<D>(layer, c[i].page, head, n_pages, n_kv_heads);
+#pragma unroll
+    for (int ps = 0; ps < kPasses; ++ps) {
+      const int t = lane / kChunksPerRow + ps * kRowsPerPass;
+      if (t >= c[i].t0) st16(blk + k_elem(t, ch), kv[i][ps]);
+      *reinterpret_cast<uint4*>(&vts[wave][i][t][ch * 8]) = vv[i][ps];
+    }
   }
   __syncthreads();
 
-  uint16_t* vdst = blk + kPageTokens * D;
 #pragma unroll
-  for (int e = lane; e < D; e += 64) {
-    uint16_t* row = vdst + e * kPageTokens;
-    if (c.t0 == 0) {
-      uint32_t w[8];
+  for (int i = 0; i < CH; ++i) {
+    if (!have[i]) continue;
+    const auto& vt = vts[wave][i];
+    uint16_t* vdst = pool + block_elem<D>(layer, c[i].page, head, n_pages, n_kv_heads) + kPageTokens * D;
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        w[j] = static_cast<uint32_t>(vt[2 * j][e]) | (static_cast<uint32_t>(vt[2 * j + 1][e]) << 16);
-      st16(row, make_uint4(w[0], w[1], w[2], w[3]));
-      st16(row + 8, make_uint4(w[4], w[5], w[6], w[7]));
-    } else {
-      for (int t = c.t0; t < kPageTokens; ++t) row[t] = vt[t][e];
+    for (int e = lane; e < D; e += 64) {
+      uint16_t* row = vdst + e * kPageTokens;
+      if (c[i].t0 == 0) {
+        uint32_t w[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          w[j] = static_cast<uint32_t>(vt[2 * j][e]) | (static_cast<uint32_t>(vt[2 * j + 1][e]) << 16);
+        st16(row, make_uint4(w[0], w[1], w[2], w[3]));
+        st16(row + 8, make_uint4(w[4], w[5], w[6], w[7]));
+      } else {
+        for (int t = c[i].t0; t < kPageTokens; ++t) row[t] = vt[t][e];
+      }
     }
+    if (c[i].new_page && blockIdx.y == 0 && threadIdx.x == 0)
+      page_table[static_cast<size_t>(c[i].slot) * max_pages + c[i].lpage] = c[i].page;
   }
-  if (c.new_page && blockIdx.y == 0 && lane == 0)
-    page_table[static_cast<size_t>(c.slot) * max_pages + c.lpage] = c.page;
 }
 
 // Zero the token slots >= valid inside 16-byte chunk i (8 elements) of a block.
@@ -154,9 +186,11 @@ hipError_t launch_append(const PoolGeom& g, const PageChunk* d_chunks, int n_chu
   if (n_chunks == 0) return hipSuccess;
   return by_dim(g.head_dim, [&](auto dc) {
     constexpr int D = decltype(dc)::value;
-    dim3 grid(n_chunks, g.n_layers * g.n_kv_heads);
-    kv_append_kernel<D><<<grid, 64, 0, stream>>>(
-        d_chunks, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), src_rows,
+    // kv heads per workgroup: 4, 2 or 1, whichever is the largest that divides n_kv_heads
+    const int waves = g.n_kv_heads % 4 == 0 ? 4 : (g.n_kv_heads % 2 == 0 ? 2 : 1);
+    dim3 grid((n_chunks + kAppendChunks - 1) / kAppendChunks, g.n_layers * (g.n_kv_heads / waves));
+    kv_append_kernel<D><<<grid, 64 * waves, 0, stream>>>(
+        d_chunks, n_chunks, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), src_rows,
         static_cast<uint16_t*>(g.pool), g.n_pages, g.n_kv_heads, g.page_table, g.max_pages);
     return hipGetLastError();
   });

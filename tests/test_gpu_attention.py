@@ -95,6 +95,42 @@ def test_decode_ragged(hq, hkv, d):
     _decode_case(hq, hkv, d, [1, 2, 15, 16, 17, 31, 32, 33, 100, 511, 512, 513, 1024, 1025, 3000])
 
 
+def test_full_pool_and_full_page_table_rows():
+    """Maximum sizes of a pool: every page allocated and every conversation at max_pages_per_conv
+    (its page-table row full); decode, extend of the last 100 tokens and turn-1 prefill of a whole
+    row all match the oracle, and one more token is refused without changing anything."""
+    from paper_2606_01839_amd import KVPool, ConserveError, CS_ERANGE, CS_ENOMEM
+    hq, hkv, d, rows, n = 32, 8, 128, 64, 4
+    L = rows * 16
+    pool = KVPool(1, hq, hkv, d, n_pages=n * rows, max_convs=n, max_pages_per_conv=rows,
+                  placement_seed=11, device="cuda")
+    convs, kvs = [], []
+    for i in range(n):
+        c = pool.conv_create()
+        kvs.append(_fill(pool, c, i, L, hkv, d))
+        convs.append(c)
+    assert pool.occupancy() == (n * rows, 0)
+    q = torch.cat([q_tokens(SEED, i, 0, L - 1, 1, hq, d) for i in range(n)]).cuda()
+    out = pool.attn_decode_batch(convs, 0, q)
+    qe = torch.cat([q_tokens(SEED, i, 0, L - 100, 100, hq, d) for i in range(n)]).cuda()
+    oe = pool.attn_extend(convs, [100] * n, 0, qe)
+    q1 = q_tokens(SEED, 0, 0, 0, L, hq, d)
+    o1 = pool.attn_prefill_turn1([convs[0]], [L], 0, q1.cuda())
+    torch.cuda.synchronize()
+    assert_close(o1, attend_last(f64(q1), f64(kvs[0][0][0]), f64(kvs[0][1][0])), "prefill of a full row")
+    for i in range(n):
+        k, v = kvs[i]
+        assert_close(out[i:i + 1], attend_last(f64(q[i:i + 1].cpu()), f64(k[0]), f64(v[0])), f"decode {i}")
+        assert_close(oe[100 * i:100 * i + 100], attend_last(f64(qe[100 * i:100 * i + 100].cpu()), f64(k[0]),
+                                                            f64(v[0])), f"extend {i}")
+    one = torch.zeros(1, 1, hkv, d, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ConserveError) as e:
+        pool.kv_append(convs[0], one, one)
+    assert e.value.code in (CS_ERANGE, CS_ENOMEM)
+    assert pool.conv_len(convs[0]) == L and pool.occupancy() == (n * rows, 0)
+    pool.close()
+
+
 def test_decode_long_contexts_few_convs():
     sk = np.linspace(0.5, 2.0, 8).astype(np.float32)
     _decode_case(32, 8, 128, [9000, 20000], scales=(sk, sk[::-1].copy()))
