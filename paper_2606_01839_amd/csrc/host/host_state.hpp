@@ -125,7 +125,7 @@ struct PageChunk {
   int32_t slot;      // page-table row
   int32_t lpage;     // logical page index within the conversation
   int32_t page;      // physical page id
-  int32_t t0, t1;    // token slots [t0, t1) of the page receive data; [t1, 16) are zeroed
+  int32_t t0, t1;    // token slots [t0, t1) of the page receive data; when t0 = 0, [t1, 16) are zeroed
   int32_t src_row;   // row (token) of the first written slot in the source tensor
   int32_t new_page;  // 1 if this page was just allocated (the mirror entry must be written)
 };

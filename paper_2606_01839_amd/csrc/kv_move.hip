@@ -12,7 +12,10 @@ namespace cs {
 // Append: one wave per (layer, kv head) and kAppendChunks page chunks, up to 4 kv heads per
 // workgroup. A wave issues the loads of all its chunks before any store (more bytes in flight per
 // wave, half as many waves), copies K pieces with 16-byte accesses, and stages V rows in LDS to
-// write them transposed. Slots [t1, 16) of each chunk's page are zeroed.
+// write them transposed. A chunk that starts a page (t0 = 0) writes the whole page, zeros in slots
+// [t1, 16); a chunk that continues a page writes only its slots [t0, t1): the rest of the page is
+// already zero, since a page's first chunk always starts at slot 0 (pages are taken as a
+// conversation crosses a 16-token boundary) and unpack writes whole pages.
 // ---------------------------------------------------------------------------------------------
 constexpr int kAppendChunks = 2;
 
@@ -68,7 +71,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const PageChunk* __restr
 #pragma unroll
     for (int ps = 0; ps < kPasses; ++ps) {
       const int t = lane / kChunksPerRow + ps * kRowsPerPass;
-      if (t >= c[i].t0) st16(blk + k_elem(t, ch), kv[i][ps]);
+      if (t >= c[i].t0 && (t < c[i].t1 || c[i].t0 == 0)) st16(blk + k_elem(t, ch), kv[i][ps]);
       *reinterpret_cast<uint4*>(&vts[wave][i][t][ch * 8]) = vv[i][ps];
     }
   }
@@ -90,7 +93,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const PageChunk* __restr
         st16(row, make_uint4(w[0], w[1], w[2], w[3]));
         st16(row + 8, make_uint4(w[4], w[5], w[6], w[7]));
       } else {
-        for (int t = c[i].t0; t < kPageTokens; ++t) row[t] = vt[t][e];
+        for (int t = c[i].t0; t < c[i].t1; ++t) row[t] = vt[t][e];
       }
     }
     if (c[i].new_page && blockIdx.y == 0 && threadIdx.x == 0)
