@@ -140,6 +140,33 @@ def blas_threads() -> int:
     return len(os.sched_getaffinity(0))
 
 
+def sample_rows(n: int, seed: int, k: int = 4):
+    """Query rows 0 .. n-1 to check and time: first and last, rows around the 16-token page and
+    64-row tile boundaries nearest the middle, and k seeded random rows (sorted, distinct)."""
+    mid = n // 2
+    rows = {0, n - 1, (mid // 16) * 16, (mid // 16) * 16 - 1, (mid // 64) * 64 + 63}
+    rows |= set(int(x) for x in np.random.default_rng(seed).integers(0, n, size=k))
+    return sorted(r for r in rows if 0 <= r < n)
+
+
+def oracle_rows(kv, q_rows, out_rows, pos, hq, d):
+    """The fp64 oracle on sampled query rows of one conversation (inputs already fp64 on the
+    host): (max abs error of the GPU rows, oracle seconds, algorithmic FLOPs of those rows)."""
+    from oracle.attention import attend_rows
+    qf = sv.bf16_to_f64(q_rows)
+    t = time.perf_counter()
+    ref = attend_rows(qf, pos, kv[0], kv[1])
+    secs = time.perf_counter() - t
+    err = float(np.abs(sv.bf16_to_f64(out_rows) - ref).max())
+    return err, secs, sum(4 * d * hq * (int(p) + 1) for p in pos)
+
+
+def oracle_baseline(flops, secs, total_flops, sample):
+    rate = flops / secs
+    return {"value": rate / 1e12, "unit": "TFLOP/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": sample, "full_batch_s_extrapolated": total_flops / rate}
+
+
 # ------------------------------------------------------------------------------------------------
 # workload construction (shared with tests/test_gpu_fullsize.py)
 # ------------------------------------------------------------------------------------------------
@@ -338,16 +365,21 @@ def bench_extend(args):
     fwd_ms = prof["attn_fwd"][0] / max(1, prof["attn_fwd"][1])
     flops = attn_flops(prefix, chunk, hq, d)
     app_bytes = 2 * int(chunk.sum()) * 2 * hkv * d * 2    # read + write of the new K and V
-    # light parity: the last query row of the first and last conversations
-    from oracle.attention import attend_rows
-    ok = True
+    # parity on sampled rows of the first and last conversations, and the oracle's time on them
+    err, secs, s_flops, n_rows = 0.0, 0.0, 0, 0
     for b in (0, tr.n_convs - 1):
-        L = int(total[b])
-        kf, vf = (sv.bf16_to_f64(t) for t in gen_kv(tr.seed, b, 0, L, hkv, d, device="cpu"))
-        row = int(chunk[:b + 1].sum()) - 1
-        ref = attend_rows(sv.bf16_to_f64(q[row:row + 1]), [L - 1], kf, vf)
-        err = np.abs(sv.bf16_to_f64(out[row:row + 1]) - ref).max()
-        ok = ok and err <= 1e-2
+        L, P, n = int(total[b]), int(prefix[b]), int(chunk[b])
+        kv = tuple(sv.bf16_to_f64(t) for t in gen_kv(tr.seed, b, 0, L, hkv, d, device="cpu"))
+        r0 = int(chunk[:b].sum())
+        rows = sample_rows(n, tr.seed + b)
+        e, t, f = oracle_rows(kv, q[[r0 + i for i in rows]], out[[r0 + i for i in rows]],
+                              [P + i for i in rows], hq, d)
+        err, secs, s_flops, n_rows = max(err, e), secs + t, s_flops + f, n_rows + len(rows)
+        del kv
+    ok = err <= 1e-2
+    cpu = oracle_baseline(s_flops, secs, flops, f"fp64 oracle on {n_rows} sampled query rows (all {hq} "
+                          f"heads) of conversations 0 and {tr.n_convs - 1}, {secs:.1f} s; the full "
+                          f"batch time is extrapolated at that rate")
     pool.close()
     del kcat, vcat
     torch.cuda.empty_cache()
@@ -360,7 +392,7 @@ def bench_extend(args):
                    "roofline": {"bound": "mfma", "achieved": flops / (fwd_ms * 1e-3) / 1e12,
                                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                                 "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
-                   "spot_parity_ok": bool(ok)},
+                   "spot_parity_ok": bool(ok), "spot_max_abs": err, "cpu_oracle": cpu},
         "append": {"workload": f"kv_append of the {int(chunk.sum())} new tokens of the extend batch",
                    "kernel_ms": app[0], "bytes": app_bytes,
                    "gbs": app_bytes / (app[0] * 1e-3) / 1e9,
@@ -440,6 +472,21 @@ def bench_prefill_transfer(args):
     fwd_ms = prof["attn_fwd"][0] / max(1, prof["attn_fwd"][1])
     flops = attn_flops([0] * len(lens), lens, hq, d)
     en = energy_run(step) if args.energy else None
+    # parity on sampled rows of the two shortest conversations, and the oracle's time on them
+    row0 = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+    err, secs, s_flops, n_rows = 0.0, 0.0, 0, 0
+    picks = [int(b) for b in np.argsort(lens, kind="stable")[:2]]
+    for b in picks:
+        L = int(lens[b])
+        kv = tuple(sv.bf16_to_f64(t) for t in gen_kv(tr.seed, b, 0, L, hkv, d, device="cpu"))
+        rows = sample_rows(L, tr.seed + b)
+        e, t, f = oracle_rows(kv, q[[int(row0[b]) + i for i in rows]], out[[int(row0[b]) + i for i in rows]],
+                              rows, hq, d)
+        err, secs, s_flops, n_rows = max(err, e), secs + t, s_flops + f, n_rows + len(rows)
+        del kv
+    cpu = oracle_baseline(s_flops, secs, flops, f"fp64 oracle on {n_rows} sampled query rows (all {hq} "
+                          f"heads) of conversations {picks[0]} and {picks[1]} (the two shortest), "
+                          f"{secs:.1f} s; the full batch time is extrapolated at that rate")
     chunked = chunked_prefill(tr, lens, q, out, mk)
     # one-time transfer: pack every conversation, unpack into a pool with other placement
     dst = mk(tr.dst_seed)
@@ -468,7 +515,8 @@ def bench_prefill_transfer(args):
                     "tflops": flops / (ms * 1e-3) / 1e12,
                     "roofline": {"bound": "mfma", "achieved": flops / (fwd_ms * 1e-3) / 1e12,
                                  "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                                 "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS}},
+                                 "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
+                    "spot_parity_ok": bool(err <= 1e-2), "spot_max_abs": err, "cpu_oracle": cpu},
         "prefill_energy": None if not en or not en["avg_watts"] else {
             **en, "tokens_per_joule": en["calls"] * int(lens.sum()) / en["wall_s"] / en["avg_watts"],
             "tflop_per_joule": en["calls"] * flops / 1e12 / en["wall_s"] / en["avg_watts"]},
