@@ -186,7 +186,9 @@ cs_status cs_attn_decode_batch(cs_pool* pool, int32_t n_convs, const cs_conv* co
  *   layer l-1 shares one launch with the decode split of layer l (two partial buffers alternate).
  * flags = CS_MIXED_LAYER_ORDERED: the order of a model forward pass, where layer l+1's queries
  *   depend on layer l's output: layer l's extend and decode overlap each other, and layer l+1
- *   starts only when both are complete.
+ *   starts only when both are complete. At head_dim 128 with both parts present, a layer is one
+ *   launch holding its extend tiles and its decode split, then the decode merge; otherwise the
+ *   layer's extend runs on the second stream beside its decode.
  * Outputs are bitwise the same either way (and the same as the separate calls).
  * Errors: as cs_kv_append_batch, cs_attn_extend and cs_attn_decode_batch; CS_EINVAL for unknown
  * flags.
@@ -236,7 +238,8 @@ enum {
   CS_PROF_DECODE_SPLIT = 3,  /* decode split-K kernel */
   CS_PROF_DECODE_MERGE = 4,  /* decode merge kernel */
   CS_PROF_ATTN_FWD = 5,      /* prefill / extend attention kernel */
-  CS_PROF_KINDS = 6
+  CS_PROF_MIXED_LAYER = 6,   /* one layer's extend tiles + decode split in one launch */
+  CS_PROF_KINDS = 7
 };
 cs_status cs_profile_start(cs_pool* pool);
 cs_status cs_profile_stop(cs_pool* pool, double* ms, int64_t* launches);

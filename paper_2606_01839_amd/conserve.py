@@ -34,7 +34,7 @@ EXPORTS = [
     "cs_place_least_occupied", "cs_sched_create", "cs_sched_destroy", "cs_sched_admit",
     "cs_sched_bind",
 ]
-PROFILE_KINDS = ["append", "pack", "unpack", "decode_split", "decode_merge", "attn_fwd"]
+PROFILE_KINDS = ["append", "pack", "unpack", "decode_split", "decode_merge", "attn_fwd", "mixed_layer"]
 
 
 class ConserveError(RuntimeError):

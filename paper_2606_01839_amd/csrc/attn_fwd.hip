@@ -21,6 +21,7 @@
 // ahead. In both, diagonal tiles apply the causal mask and fully visible tiles skip it.
 #include <cmath>
 
+#include "decode_split.hpp"
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -90,9 +91,9 @@ __device__ __forceinline__ void dma_wait_barrier() {
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" :: "n"(N) : "memory");
 }
 
+// One (tile, kv head) workgroup of the head_dim 128 kernel (`block` = its index in the grid).
 template <int G>
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
-void attn_fwd_kernel(ExtendArgs a) {
+__device__ __forceinline__ void attn_fwd_block(const ExtendArgs& a, const int block) {
   constexpr int D = 128;
   constexpr int NW = 8;                   // waves: G query heads x (8 / G) blocks of 32 queries
   constexpr int BM = 32 * (NW / G);       // queries per workgroup
@@ -107,7 +108,7 @@ void attn_fwd_kernel(ExtendArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NBUF * TILE];
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int tile_idx = blockIdx.x / a.n_kv_heads, g = blockIdx.x % a.n_kv_heads;
+  const int tile_idx = block / a.n_kv_heads, g = block % a.n_kv_heads;
   const ExtendTile tile = a.tiles[tile_idx];
   const ExtendConvDesc cd = a.convs[tile.conv];
   const int prefix = cd.len - cd.q_len;
@@ -324,6 +325,27 @@ void attn_fwd_kernel(ExtendArgs a) {
                                    pack_bf16x2(o[t][4 * e4 + 2] * inv, o[t][4 * e4 + 3] * inv)));
       }
   }
+}
+
+template <int G>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_fwd_kernel(ExtendArgs a) {
+  attn_fwd_block<G>(a, blockIdx.x);
+}
+
+// One layer of a mixed step in one launch (head_dim 128): the first n_ext workgroups are the
+// extend tiles of the layer, the others each run two 4-wave groups of the layer's decode split.
+// Every workgroup gets the attention kernel's LDS ring and register budget (one per CU, two waves
+// per SIMD); the decode split reads HBM as fast with two waves per SIMD as with three.
+template <int G>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
+void mixed_layer_kernel(ExtendArgs ea, int n_ext, DecodeArgs da) {
+  if (static_cast<int>(blockIdx.x) < n_ext) {
+    attn_fwd_block<G>(ea, blockIdx.x);
+    return;
+  }
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  split_body<128>(da, (blockIdx.x - n_ext) * 2 + (wave >> 2), wave & 3);
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -589,10 +611,8 @@ static void launch_fwd(const ExtendArgs& a, int n_tiles, int n_kv_heads, hipStre
 
 int extend_query_tile(int head_dim, int group) { return head_dim == 128 ? 256 / group : kBM; }
 
-hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,
-                         const ExtendTile* d_tiles, int n_tiles, const void* q, void* out,
-                         hipStream_t stream) {
-  if (n_tiles == 0) return hipSuccess;
+static ExtendArgs make_extend_args(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,
+                                   const ExtendTile* d_tiles, const void* q, void* out) {
   ExtendArgs a;
   a.pool = static_cast<const uint16_t*>(g.pool);
   a.n_pages = g.n_pages;
@@ -605,6 +625,14 @@ hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_c
   a.q = static_cast<const uint16_t*>(q);
   a.out = static_cast<uint16_t*>(out);
   a.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(g.head_dim)));
+  return a;
+}
+
+hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_convs,
+                         const ExtendTile* d_tiles, int n_tiles, const void* q, void* out,
+                         hipStream_t stream) {
+  if (n_tiles == 0) return hipSuccess;
+  const ExtendArgs a = make_extend_args(g, layer, d_convs, d_tiles, q, out);
   const int G = g.n_q_heads / g.n_kv_heads;
 #define CS_FWD_CASE(DD, GG)                                   \
   if (g.head_dim == DD && G == GG) {                          \
@@ -615,6 +643,27 @@ hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_c
   CS_FWD_CASE(64, 1) CS_FWD_CASE(64, 2) CS_FWD_CASE(64, 4) CS_FWD_CASE(64, 8)
 #undef CS_FWD_CASE
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_mixed_layer(const PoolGeom& g, int layer, const ExtendConvDesc* d_ext_convs,
+                              const ExtendTile* d_tiles, int n_tiles, const void* q_ext,
+                              void* out_ext, const DecodeConvDesc* d_dec_convs, int n_dec_convs,
+                              int n_items, int split_tokens, const void* q_dec, float* partials,
+                              hipStream_t stream) {
+  if (g.head_dim != 128 || n_tiles == 0 || n_dec_convs == 0) return hipErrorInvalidValue;
+  const ExtendArgs ea = make_extend_args(g, layer, d_ext_convs, d_tiles, q_ext, out_ext);
+  const DecodeArgs da = make_decode_args(g, layer, d_dec_convs, n_dec_convs, n_items, split_tokens,
+                                         q_dec, nullptr, partials);
+  const int n_ext = n_tiles * g.n_kv_heads;
+  const int blocks = n_ext + (n_items * g.n_kv_heads + 7) / 8;
+  switch (g.n_q_heads / g.n_kv_heads) {
+    case 1: mixed_layer_kernel<1><<<blocks, 512, 0, stream>>>(ea, n_ext, da); break;
+    case 2: mixed_layer_kernel<2><<<blocks, 512, 0, stream>>>(ea, n_ext, da); break;
+    case 4: mixed_layer_kernel<4><<<blocks, 512, 0, stream>>>(ea, n_ext, da); break;
+    case 8: mixed_layer_kernel<8><<<blocks, 512, 0, stream>>>(ea, n_ext, da); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace cs

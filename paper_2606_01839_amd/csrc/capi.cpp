@@ -790,6 +790,24 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
     CS_HIP(hipStreamWaitEvent(p->stream, p->join_ev, 0), "hipStreamWaitEvent");
     return CS_OK;
   };
+  if ((flags & CS_MIXED_LAYER_ORDERED) && fork && p->desc.head_dim == 128 && ew.parts.size() == 1) {
+    // As in a model forward pass, one layer after the other; each layer is one launch with its
+    // extend tiles and its decode split, then the decode merge.
+    const cs::PoolGeom g = p->geom();
+    const auto& pw = ew.parts[0];
+    for (int layer = 0; layer < nl && st == CS_OK; ++layer) {
+      st = timed_launch(p, CS_PROF_MIXED_LAYER, "mixed layer launch", [&] {
+        return cs::launch_mixed_layer(g, layer, pw.convs, pw.tiles, pw.n_tiles, q_e(layer), o_e(layer),
+                                      dw.convs, dw.n_convs, dw.n_items, dw.split, q_d(layer),
+                                      p->partials(), p->stream);
+      });
+      if (st == CS_OK)
+        st = timed_launch(p, CS_PROF_DECODE_MERGE, "decode merge launch", [&] {
+          return cs::launch_decode_merge(g, dw.convs, dw.n_convs, p->partials(), o_d(layer), p->stream);
+        });
+    }
+    return st;
+  }
   if (flags & CS_MIXED_LAYER_ORDERED) {
     // As in a model forward pass: layer l's extend and decode overlap each other, and layer l+1
     // starts only once both are complete.

@@ -47,6 +47,14 @@ hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const D
                                      float* split_partials, const float* merge_partials,
                                      void* merge_out, hipStream_t stream);
 
+// One layer of a mixed step in one launch (head_dim 128 only): the extend tiles of the layer and
+// its decode split (partials; the merge follows as launch_decode_merge).
+hipError_t launch_mixed_layer(const PoolGeom& g, int layer, const ExtendConvDesc* d_ext_convs,
+                              const ExtendTile* d_tiles, int n_tiles, const void* q_ext,
+                              void* out_ext, const DecodeConvDesc* d_dec_convs, int n_dec_convs,
+                              int n_items, int split_tokens, const void* q_dec, float* partials,
+                              hipStream_t stream);
+
 // Query tokens per extend/prefill work tile for this head size and GQA group (the host plan must
 // match).
 int extend_query_tile(int head_dim, int group);
