@@ -38,7 +38,8 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
 METRIC = "decode-attn HBM GB/s + extend/prefill TFLOP/s, each as % of MI355X peak"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_split_traffic.json")
-KERNEL_SOURCES = ["paper_2606_01839_amd/csrc/decode.hip", "paper_2606_01839_amd/csrc/device_common.hpp"]
+KERNEL_SOURCES = ["paper_2606_01839_amd/csrc/decode.hip", "paper_2606_01839_amd/csrc/decode_split.hpp",
+                  "paper_2606_01839_amd/csrc/device_common.hpp"]
 
 
 def log(*a):
