@@ -76,7 +76,10 @@ __device__ __forceinline__ void merge_body(const DecodeArgs& a, const int b, con
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) { split_body<D>(a, blockIdx.x, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)); }
+__global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
+  __shared__ float xch[split_exchange_floats<D>()];
+  split_body<D>(a, blockIdx.x, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), xch);
+}
 
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
@@ -88,13 +91,14 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
 // l+1's split into the other partial buffer. Saves one launch and its gap per layer.
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_split_kernel(DecodeArgs am, DecodeArgs as) {
+  __shared__ float xch[split_exchange_floats<D>()];
   const int n_merge = am.n_convs * am.n_kv_heads * am.group;
   const int blk = blockIdx.x;
   if (blk < n_merge) {
     const int nqh = am.n_kv_heads * am.group;
     merge_body<D>(am, blk / nqh, blk % nqh);
   } else {
-    split_body<D>(as, blk - n_merge, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
+    split_body<D>(as, blk - n_merge, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), xch);
   }
 }
 
@@ -103,7 +107,7 @@ hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDes
                                float* partials, hipStream_t stream) {
   if (n_convs == 0) return hipSuccess;
   const DecodeArgs a = make_decode_args(g, layer, d_convs, n_convs, n_items, split_tokens, q, nullptr, partials);
-  const int blocks = (n_items * g.n_kv_heads + 3) / 4;
+  const int blocks = n_items * g.n_kv_heads;
   if (g.head_dim == 128) decode_split_kernel<128><<<blocks, 256, 0, stream>>>(a);
   else if (g.head_dim == 64) decode_split_kernel<64><<<blocks, 256, 0, stream>>>(a);
   else return hipErrorInvalidValue;
@@ -118,7 +122,7 @@ hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const D
   const DecodeArgs as = make_decode_args(g, split_layer, d_convs, n_convs, n_items, split_tokens, q, nullptr,
                                   split_partials);
   const DecodeArgs am = make_decode_args(g, 0, d_convs, n_convs, 0, 0, nullptr, merge_out, merge_partials);
-  const int blocks = n_convs * g.n_q_heads + (n_items * g.n_kv_heads + 3) / 4;
+  const int blocks = n_convs * g.n_q_heads + n_items * g.n_kv_heads;
   if (g.head_dim == 128) decode_merge_split_kernel<128><<<blocks, 256, 0, stream>>>(am, as);
   else if (g.head_dim == 64) decode_merge_split_kernel<64><<<blocks, 256, 0, stream>>>(am, as);
   else return hipErrorInvalidValue;

@@ -53,22 +53,31 @@ __device__ __forceinline__ int find_conv(const __attribute__((address_space(4)))
   return lo;
 }
 
-// Split work of one 4-wave group (`block`, this wave = `wave` in 0 .. 3): the wave takes work
-// unit block * 4 + wave = (item, kv head), reads the item's pages once and writes its partials.
+// LDS floats one 4-wave group needs to hand waves 1 .. 3's partial results to wave 0 (up to 8
+// query heads per kv head: o[D], m, l each).
 template <int D>
-__device__ __forceinline__ void split_body(const DecodeArgs& a, const int block, const int wave) {
+constexpr int split_exchange_floats() { return (kDecodeSubSplits - 1) * 8 * (D + 2); }
+
+// Work item `work` = (item, kv head) of the plan, taken by one 4-wave group (this wave = `wave` in
+// 0 .. 3; `xch` = the group's LDS exchange area, split_exchange_floats<D>() floats). Wave w reads
+// split w of the item -- keys [k0 + w split, k0 + (w + 1) split) -- once; then waves 1 .. 3 hand
+// their (o, m, l) to wave 0 through LDS, which merges the four in that order and writes the item's
+// partial record. Every wave of the workgroup reaches the one barrier, also in a group whose work
+// unit lies past the end (work >= n_items * n_kv_heads: no keys, nothing written).
+template <int D>
+__device__ __forceinline__ void split_body(const DecodeArgs& a, const int work, const int wave,
+                                           float* xch) {
   constexpr int KS = D / 32;  // k-steps of the QK^T contraction
   constexpr int DT = D / 16;  // 16-dim tiles of the output
   const int lane = threadIdx.x & 63;
-  const int work = block * 4 + wave;  // = item * n_kv_heads + kv head
-  if (work >= a.n_items * a.n_kv_heads) return;
-  const int item = work / a.n_kv_heads, g = work % a.n_kv_heads;
+  const bool valid = work < a.n_items * a.n_kv_heads;
+  const int item = valid ? work / a.n_kv_heads : 0, g = work % a.n_kv_heads;
   const auto* convs = as_const(a.convs);
   const int conv_idx = find_conv(convs, a.n_convs, item);
   const DecodeConvDesc cd = load_desc(convs + conv_idx);
-  const int k_begin = (item - cd.item_start) * a.split;
-  const int k_end = min(cd.len, k_begin + a.split);
-  const int n_pg = (k_end - k_begin + kPageTokens - 1) / kPageTokens;
+  const int k_begin = ((item - cd.item_start) * kDecodeSubSplits + wave) * a.split;
+  const int k_end = valid ? min(cd.len, k_begin + a.split) : k_begin;
+  const int n_pg = k_end > k_begin ? (k_end - k_begin + kPageTokens - 1) / kPageTokens : 0;
   const int32_t* pt = a.page_table + static_cast<size_t>(cd.slot) * a.max_pages + k_begin / kPageTokens;
 
   const int c = lane & 15;   // MFMA column: query head within the group; A-operand row: key / dim
@@ -176,15 +185,46 @@ __device__ __forceinline__ void split_body(const DecodeArgs& a, const int block,
   // l_run holds this lane's keys only; sum over the four k-blocks of the column.
   l_run += xor_shfl(l_run, 16);
   l_run += xor_shfl(l_run, 32);
-  if (c < a.group) {
+  // A wave past the conversation's end has m = -inf, l = 0, o = 0 and adds nothing below.
+  if (wave > 0 && c < a.group) {
+    float* x = xch + ((wave - 1) * 8 + c) * (D + 2);
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) x[16 * t + 4 * qd + r] = o[t][r];
+    if (qd == 0) {
+      x[D] = m_run;
+      x[D + 1] = l_run;
+    }
+  }
+  __syncthreads();
+  if (wave == 0 && valid && c < a.group) {
+    // wave 0 always holds keys, so M is finite; merge in the order w = 0, 1, 2, 3
+    float M = m_run;
+#pragma unroll
+    for (int w = 1; w < kDecodeSubSplits; ++w) M = fmaxf(M, xch[((w - 1) * 8 + c) * (D + 2) + D]);
+    const float a0 = fast_exp2(m_run - M);
+    float l = l_run * a0;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) o[t] *= a0;
+#pragma unroll
+    for (int w = 1; w < kDecodeSubSplits; ++w) {
+      const float* x = xch + ((w - 1) * 8 + c) * (D + 2);
+      const float aw = fast_exp2(x[D] - M);
+      l = __builtin_fmaf(aw, x[D + 1], l);
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[t][r] = __builtin_fmaf(aw, x[16 * t + 4 * qd + r], o[t][r]);
+    }
     float* pp = a.partials + (static_cast<size_t>(work) * a.group + c) * partial_floats(D);
 #pragma unroll
     for (int t = 0; t < DT; ++t)
 #pragma unroll
       for (int r = 0; r < 4; ++r) pp[16 * t + 4 * qd + r] = o[t][r];
     if (qd == 0) {
-      pp[D] = m_run;
-      pp[D + 1] = l_run;
+      pp[D] = M;
+      pp[D + 1] = l;
     }
   }
 }

@@ -90,10 +90,11 @@ DecodePlan plan_decode(const std::vector<int32_t>& slots, const std::vector<int6
     if (items * n_kv_heads >= target_items) break;
   }
   const int32_t split = plan.split_tokens;
+  const int64_t item_keys = static_cast<int64_t>(kDecodeSubSplits) * split;
   int32_t start = 0;
   plan.convs.reserve(lens.size());
   for (size_t i = 0; i < lens.size(); ++i) {
-    int32_t ns = static_cast<int32_t>((lens[i] + split - 1) / split);
+    int32_t ns = static_cast<int32_t>((lens[i] + item_keys - 1) / item_keys);
     plan.convs.push_back({slots[i], static_cast<int32_t>(lens[i]), start, ns});
     start += ns;
   }

@@ -81,18 +81,23 @@ class ConvTable {
 struct DecodeConvDesc {
   int32_t slot;        // row of the device page-table mirror
   int32_t len;         // tokens
-  int32_t item_start;  // first split index of this conversation
-  int32_t n_splits;
+  int32_t item_start;  // first work item of this conversation
+  int32_t n_splits;    // work items: ceil(len / (kDecodeSubSplits * split_tokens))
 };
 
+// Waves per decode work item: each takes one split of keys; the item's waves merge their partial
+// results on chip and write one partial record per query head.
+constexpr int kDecodeSubSplits = 4;
+
 struct DecodePlan {
-  int32_t split_tokens = 0;  // multiple of 32, <= 1024
-  int32_t n_items = 0;       // total splits over the batch (per kv head)
+  int32_t split_tokens = 0;  // keys per wave (one split), multiple of 32, <= 1024
+  int32_t n_items = 0;       // work items over the batch (per kv head)
   std::vector<DecodeConvDesc> convs;
 };
 
-// Choose the split size: the largest candidate that still yields at least `target_items` work
-// items across kv heads, else the smallest candidate.
+// Choose the split size: the largest candidate for which the splits holding keys, over all kv
+// heads, number at least `target_items` (the waves that read), else the smallest candidate. A
+// work item is kDecodeSubSplits consecutive splits of one conversation.
 DecodePlan plan_decode(const std::vector<int32_t>& slots, const std::vector<int64_t>& lens,
                        int32_t n_kv_heads, int64_t target_items);
 

@@ -58,10 +58,14 @@ static void decode_plan() {
   std::vector<int64_t> lens = {1, 1000, 4096};
   cs::DecodePlan p = cs::plan_decode(slots, lens, 8, 1 << 30);  // unreachable target -> smallest split
   CHECK(p.split_tokens == 128);
-  CHECK(p.convs.size() == 3 && p.convs[0].n_splits == 1 && p.convs[1].n_splits == 8 && p.convs[2].n_splits == 32);
-  CHECK(p.convs[1].item_start == 1 && p.convs[2].item_start == 9 && p.n_items == 41);
+  // work items of kDecodeSubSplits = 4 splits of 128 keys: ceil(L / 512)
+  CHECK(p.convs.size() == 3 && p.convs[0].n_splits == 1 && p.convs[1].n_splits == 2 && p.convs[2].n_splits == 8);
+  CHECK(p.convs[1].item_start == 1 && p.convs[2].item_start == 3 && p.n_items == 11);
   cs::DecodePlan q = cs::plan_decode(slots, lens, 8, 1);  // any split satisfies -> largest
-  CHECK(q.split_tokens == 1024 && q.n_items == 1 + 1 + 4);
+  CHECK(q.split_tokens == 1024 && q.n_items == 1 + 1 + 1);
+  // the target counts splits holding keys: 1 + 1 + 4 = 6 splits of 1024 keys, x 8 kv heads = 48
+  CHECK(cs::plan_decode(slots, lens, 8, 48).split_tokens == 1024);
+  CHECK(cs::plan_decode(slots, lens, 8, 49).split_tokens == 512);
 }
 
 static void extend_plan() {
