@@ -334,20 +334,20 @@ void attn_fwd_kernel(ExtendArgs a) {
 }
 
 // One layer of a mixed step in one launch (head_dim 128): the first n_ext workgroups are the
-// extend tiles of the layer, the others each run two 4-wave groups of the layer's decode split.
-// Every workgroup gets the attention kernel's LDS ring and register budget (one per CU, two waves
-// per SIMD); the decode split reads HBM as fast with two waves per SIMD as with three. Both 4-wave
-// groups of a decode workgroup pass the split's one barrier.
+// extend tiles of the layer, the others each take one work item of the layer's decode split (8
+// waves, as in the split kernel). Every workgroup gets the attention kernel's LDS ring and register
+// budget (one per CU, two waves per SIMD); the decode split reads HBM as fast with two waves per
+// SIMD as with three.
 template <int G>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
 void mixed_layer_kernel(ExtendArgs ea, int n_ext, DecodeArgs da) {
-  __shared__ float xch[2][split_exchange_floats<128>()];
+  static_assert(kDecodeItemThreads == 512, "a decode work item fills one attention workgroup");
+  __shared__ float xch[split_exchange_floats<128>()];
   if (static_cast<int>(blockIdx.x) < n_ext) {
     attn_fwd_block<G>(ea, blockIdx.x);
     return;
   }
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  split_body<128>(da, (blockIdx.x - n_ext) * 2 + (wave >> 2), wave & 3, xch[wave >> 2]);
+  split_body<128>(da, blockIdx.x - n_ext, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), xch);
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -657,7 +657,7 @@ hipError_t launch_mixed_layer(const PoolGeom& g, int layer, const ExtendConvDesc
   const DecodeArgs da = make_decode_args(g, layer, d_dec_convs, n_dec_convs, n_items, split_tokens,
                                          q_dec, nullptr, partials);
   const int n_ext = n_tiles * g.n_kv_heads;
-  const int blocks = n_ext + (n_items * g.n_kv_heads + 1) / 2;
+  const int blocks = n_ext + n_items * g.n_kv_heads;
   switch (g.n_q_heads / g.n_kv_heads) {
     case 1: mixed_layer_kernel<1><<<blocks, 512, 0, stream>>>(ea, n_ext, da); break;
     case 2: mixed_layer_kernel<2><<<blocks, 512, 0, stream>>>(ea, n_ext, da); break;

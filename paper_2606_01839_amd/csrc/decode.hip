@@ -19,34 +19,40 @@
 
 namespace cs {
 
-// One workgroup per (conversation, query head): log-sum-exp merge of its splits, in three steps
-// whose order depends only on the split count (bitwise deterministic): the maximum M of the split
-// maxima; per thread, the weighted sum over a fixed subset of the splits (split group sg = thread /
-// (D/4) takes splits sg, sg + SG, ...; dim group = 4 consecutive dims, one 16-byte load); then the
-// split groups added in order 0 .. SG-1.
+// Log-sum-exp merge of the item records of one (conversation b, query head h) by 256 threads (`tid`
+// in 0 .. 255, LDS `lds`), in three steps whose order depends only on the record count (bitwise
+// deterministic): the maximum M of the record maxima; per thread, the weighted sum over a fixed
+// subset of the records (group sg = tid / (D/4) takes records sg, sg + SG, ...; dim group = 4
+// consecutive dims, one 16-byte load); then the groups added in order 0 .. SG-1. With valid =
+// false the threads only pass the two barriers.
 template <int D>
-__device__ __forceinline__ void merge_body(const DecodeArgs& a, const int b, const int h) {
+struct MergeLds {
+  float red_o[256 / (D / 4)][D];
+  float red_l[256 / (D / 4)];
+  float wave_max[4];
+};
+
+template <int D>
+__device__ __forceinline__ void merge_body(const DecodeArgs& a, const int b, const int h, const int tid,
+                                           MergeLds<D>& lds, const bool valid) {
   constexpr int DV = D / 4;          // dim groups (4 dims each)
-  constexpr int SG = 256 / DV;       // split groups
+  constexpr int SG = 256 / DV;       // record groups
   constexpr int R = partial_floats(D);
-  __shared__ float red_o[SG][D];
-  __shared__ float red_l[SG];
-  __shared__ float wave_max[4];
   const int g = h / a.group, c = h % a.group;
-  const DecodeConvDesc cd = load_desc(as_const(a.convs) + b);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const DecodeConvDesc cd = load_desc(as_const(a.convs) + (valid ? b : 0));
+  const int lane = tid & 63, wave = tid >> 6;
   const size_t split_stride = static_cast<size_t>(a.n_kv_heads) * a.group * R;
   const float* base =
       a.partials + ((static_cast<size_t>(cd.item_start) * a.n_kv_heads + g) * a.group + c) * R;
-  const int n = cd.n_splits;
+  const int n = valid ? cd.n_splits : 0;
 
   float M = -INFINITY;
   for (int s = tid; s < n; s += 256) M = fmaxf(M, base[s * split_stride + D]);
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, xor_shfl(M, off));
-  if (lane == 0) wave_max[wave] = M;
+  if (lane == 0) lds.wave_max[wave] = M;
   __syncthreads();
-  M = fmaxf(fmaxf(wave_max[0], wave_max[1]), fmaxf(wave_max[2], wave_max[3]));
+  M = fmaxf(fmaxf(lds.wave_max[0], lds.wave_max[1]), fmaxf(lds.wave_max[2], lds.wave_max[3]));
 
   const int dg = tid % DV, sg = tid / DV;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -60,15 +66,15 @@ __device__ __forceinline__ void merge_body(const DecodeArgs& a, const int b, con
     acc += w * v;
     den += w * ml.y;
   }
-  *reinterpret_cast<f32x4*>(&red_o[sg][4 * dg]) = acc;
-  if (dg == 0) red_l[sg] = den;
+  *reinterpret_cast<f32x4*>(&lds.red_o[sg][4 * dg]) = acc;
+  if (dg == 0) lds.red_l[sg] = den;
   __syncthreads();
-  if (tid < D) {
+  if (valid && tid < D) {
     float o = 0.f, l = 0.f;
 #pragma unroll
     for (int k = 0; k < SG; ++k) {
-      o += red_o[k][tid];
-      l += red_l[k];
+      o += lds.red_o[k][tid];
+      l += lds.red_l[k];
     }
     uint16_t* orow = a.out + (static_cast<size_t>(b) * a.n_kv_heads * a.group + h) * D;
     orow[tid] = static_cast<uint16_t>(pack_bf16x2(o / l, 0.f) & 0xFFFFu);
@@ -76,29 +82,35 @@ __device__ __forceinline__ void merge_body(const DecodeArgs& a, const int b, con
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kDecodeItemThreads) void decode_split_kernel(DecodeArgs a) {
   __shared__ float xch[split_exchange_floats<D>()];
   split_body<D>(a, blockIdx.x, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), xch);
 }
 
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
-  merge_body<D>(a, blockIdx.x, blockIdx.y);
+  __shared__ MergeLds<D> lds;
+  merge_body<D>(a, blockIdx.x, blockIdx.y, threadIdx.x, lds, true);
 }
 
 // The merge of one layer and the split of the next in one launch (a multi-layer step): the first
-// n_conv * n_q_heads workgroups merge layer l's partials (buffer am.partials), the others run layer
-// l+1's split into the other partial buffer. Saves one launch and its gap per layer.
+// workgroups merge layer l's partials (buffer am.partials), kDecodeItemThreads / 256 (conversation,
+// query head) pairs each, the others run layer l+1's split into the other partial buffer. Saves
+// one launch and its gap per layer.
 template <int D>
-__global__ __launch_bounds__(256) void decode_merge_split_kernel(DecodeArgs am, DecodeArgs as) {
+__global__ __launch_bounds__(kDecodeItemThreads) void decode_merge_split_kernel(DecodeArgs am, DecodeArgs as,
+                                                                                int merge_blocks) {
+  constexpr int kPerBlock = kDecodeItemThreads / 256;
   __shared__ float xch[split_exchange_floats<D>()];
-  const int n_merge = am.n_convs * am.n_kv_heads * am.group;
+  __shared__ MergeLds<D> lds[kPerBlock];
   const int blk = blockIdx.x;
-  if (blk < n_merge) {
+  if (blk < merge_blocks) {
     const int nqh = am.n_kv_heads * am.group;
-    merge_body<D>(am, blk / nqh, blk % nqh);
+    const int part = threadIdx.x >> 8, pair = blk * kPerBlock + part;
+    const bool valid = pair < am.n_convs * nqh;
+    merge_body<D>(am, valid ? pair / nqh : 0, valid ? pair % nqh : 0, threadIdx.x & 255, lds[part], valid);
   } else {
-    split_body<D>(as, blk - n_merge, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), xch);
+    split_body<D>(as, blk - merge_blocks, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), xch);
   }
 }
 
@@ -108,8 +120,8 @@ hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDes
   if (n_convs == 0) return hipSuccess;
   const DecodeArgs a = make_decode_args(g, layer, d_convs, n_convs, n_items, split_tokens, q, nullptr, partials);
   const int blocks = n_items * g.n_kv_heads;
-  if (g.head_dim == 128) decode_split_kernel<128><<<blocks, 256, 0, stream>>>(a);
-  else if (g.head_dim == 64) decode_split_kernel<64><<<blocks, 256, 0, stream>>>(a);
+  if (g.head_dim == 128) decode_split_kernel<128><<<blocks, kDecodeItemThreads, 0, stream>>>(a);
+  else if (g.head_dim == 64) decode_split_kernel<64><<<blocks, kDecodeItemThreads, 0, stream>>>(a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -122,9 +134,13 @@ hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const D
   const DecodeArgs as = make_decode_args(g, split_layer, d_convs, n_convs, n_items, split_tokens, q, nullptr,
                                   split_partials);
   const DecodeArgs am = make_decode_args(g, 0, d_convs, n_convs, 0, 0, nullptr, merge_out, merge_partials);
-  const int blocks = n_convs * g.n_q_heads + n_items * g.n_kv_heads;
-  if (g.head_dim == 128) decode_merge_split_kernel<128><<<blocks, 256, 0, stream>>>(am, as);
-  else if (g.head_dim == 64) decode_merge_split_kernel<64><<<blocks, 256, 0, stream>>>(am, as);
+  constexpr int kPerBlock = kDecodeItemThreads / 256;
+  const int merge_blocks = (n_convs * g.n_q_heads + kPerBlock - 1) / kPerBlock;
+  const int blocks = merge_blocks + n_items * g.n_kv_heads;
+  if (g.head_dim == 128)
+    decode_merge_split_kernel<128><<<blocks, kDecodeItemThreads, 0, stream>>>(am, as, merge_blocks);
+  else if (g.head_dim == 64)
+    decode_merge_split_kernel<64><<<blocks, kDecodeItemThreads, 0, stream>>>(am, as, merge_blocks);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

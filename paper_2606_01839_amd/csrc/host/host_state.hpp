@@ -87,7 +87,7 @@ struct DecodeConvDesc {
 
 // Waves per decode work item: each takes one split of keys; the item's waves merge their partial
 // results on chip and write one partial record per query head.
-constexpr int kDecodeSubSplits = 4;
+constexpr int kDecodeSubSplits = 8;
 
 struct DecodePlan {
   int32_t split_tokens = 0;  // keys per wave (one split), multiple of 32, <= 1024

@@ -58,11 +58,13 @@ static void decode_plan() {
   std::vector<int64_t> lens = {1, 1000, 4096};
   cs::DecodePlan p = cs::plan_decode(slots, lens, 8, 1 << 30);  // unreachable target -> smallest split
   CHECK(p.split_tokens == 128);
-  // work items of kDecodeSubSplits = 4 splits of 128 keys: ceil(L / 512)
-  CHECK(p.convs.size() == 3 && p.convs[0].n_splits == 1 && p.convs[1].n_splits == 2 && p.convs[2].n_splits == 8);
-  CHECK(p.convs[1].item_start == 1 && p.convs[2].item_start == 3 && p.n_items == 11);
+  // work items of kDecodeSubSplits splits of 128 keys each
+  const int64_t ik = static_cast<int64_t>(cs::kDecodeSubSplits) * 128;
+  const int32_t n1 = static_cast<int32_t>((1000 + ik - 1) / ik), n2 = static_cast<int32_t>((4096 + ik - 1) / ik);
+  CHECK(p.convs.size() == 3 && p.convs[0].n_splits == 1 && p.convs[1].n_splits == n1 && p.convs[2].n_splits == n2);
+  CHECK(p.convs[1].item_start == 1 && p.convs[2].item_start == 1 + n1 && p.n_items == 1 + n1 + n2);
   cs::DecodePlan q = cs::plan_decode(slots, lens, 8, 1);  // any split satisfies -> largest
-  CHECK(q.split_tokens == 1024 && q.n_items == 1 + 1 + 1);
+  CHECK(q.split_tokens == 1024 && q.n_items == 3);         // one item each (4096 <= 4 * 1024)
   // the target counts splits holding keys: 1 + 1 + 4 = 6 splits of 1024 keys, x 8 kv heads = 48
   CHECK(cs::plan_decode(slots, lens, 8, 48).split_tokens == 1024);
   CHECK(cs::plan_decode(slots, lens, 8, 49).split_tokens == 512);
