@@ -1,18 +1,20 @@
 // Batched single-token decode attention over paged KV (split-K "flash decoding").
 //
-// Work item = (conversation, logical split of `split` keys, kv head): one wave reads the split's
-// pages once and serves all G query heads of the kv head. The two contractions per page pair are
-// done on the matrix cores with v_mfma_f32_16x16x32_bf16, the GQA group as the 16-wide N side:
+// One wave reads one split (`split` consecutive keys) of one (conversation, kv head) once and
+// serves all G query heads of the kv head; a work item is kDecodeSubSplits consecutive splits, one
+// workgroup. The two contractions per page pair are done on the matrix cores with
+// v_mfma_f32_16x16x32_bf16, the GQA group as the 16-wide N side:
 //   S^T[key][head] = K[key][:] . Q[head][:]          (A = K rows straight from the page,
 //                                                     B = Q, 8 consecutive dims per lane)
 //   O^T[dim][head] += V^T[dim][key] . P^T[key][head]  (A = V^T rows from the page,
 //                                                     B = P from the S^T accumulator registers)
-// so K and V^T are used in the layout they are stored in (no LDS): each K operand load reads one
-// 1 KiB sub-block of a page, each V^T load 512 consecutive bytes.
-// The softmax is online in fp32 (exp2 with log2(e)/sqrt(d) folded into the score scale); the
-// per-item partial (o, m, l) goes to a workspace and a second kernel merges the splits of each
-// (conversation, query head) in a fixed order. No atomics: bitwise deterministic, and split
-// boundaries are logical positions, so results do not depend on physical page placement.
+// so K and V^T are used in the layout they are stored in: each K operand load reads one 1 KiB
+// sub-block of a page, each V^T load 512 consecutive bytes. The softmax is online in fp32 (exp2
+// with log2(e)/sqrt(d) folded into the score scale). The waves of an item merge their (o, m, l) in
+// LDS and write one partial record per (item, query head) to a workspace (decode_split.hpp); a
+// second kernel merges the items of each (conversation, query head). Both merges run in a fixed
+// order and there are no atomics: bitwise deterministic, and split boundaries are logical
+// positions, so results do not depend on physical page placement.
 #include <cmath>
 
 #include "decode_split.hpp"

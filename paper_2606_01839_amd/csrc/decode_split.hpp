@@ -19,11 +19,11 @@ struct DecodeArgs {
   int max_pages;
   const DecodeConvDesc* convs;
   int n_convs;
-  int n_items;
-  int split;  // keys per split, multiple of 32, <= 1024
+  int n_items;  // work items of the plan (kDecodeSubSplits splits each)
+  int split;    // keys per split (per wave), multiple of 32, <= 1024
   const uint16_t* q;
   uint16_t* out;
-  float* partials;  // [n_items * n_kv_heads][group] records of partial_floats(D)
+  float* partials;  // [n_items * n_kv_heads][group] records of partial_floats(D), one per item
   float scale_log2;
 };
 
