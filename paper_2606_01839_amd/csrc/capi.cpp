@@ -28,7 +28,9 @@ constexpr size_t kAlign = 256;
 constexpr size_t kRingBytes = size_t(8) << 20;  // metadata ring (device + pinned host), 4 quarters
 constexpr size_t kQuarter = kRingBytes / 4;
 constexpr int kMinSplit = 128;                   // smallest decode split: bounds the partials
-constexpr int64_t kDecodeTargetItems = 4096;     // work items a decode launch aims for
+// Splits (waves) a decode launch aims for (16 per CU). Half as many (longer splits, fewer items to
+// merge) made the 32-layer mixed trace 5% slower.
+constexpr int64_t kDecodeTargetItems = 4096;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -399,6 +401,7 @@ cs_status launch_extend_layer(cs_pool* p, const ExtendWork& w, int layer, const 
 struct DecodeWork {
   cs::DecodeConvDesc* convs = nullptr;
   int n_convs = 0, n_items = 0, split = 0;
+  bool single = false;  // one work item per conversation: the split writes the output directly
 };
 
 cs_status upload_decode(cs_pool* p, const std::vector<int32_t>& slots, const std::vector<int64_t>& lens,
@@ -412,16 +415,18 @@ cs_status upload_decode(cs_pool* p, const std::vector<int32_t>& slots, const std
   w->n_convs = static_cast<int>(plan.convs.size());
   w->n_items = plan.n_items;
   w->split = plan.split_tokens;
+  w->single = plan.single_item;
   return CS_OK;
 }
 
+// Split, then merge; when every conversation is one work item the split writes the output itself.
 cs_status launch_decode_layer(cs_pool* p, const DecodeWork& w, int layer, const void* q, void* out) {
   const cs::PoolGeom g = p->geom();
   cs_status st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
     return cs::launch_decode_split(g, layer, w.convs, w.n_convs, w.n_items, w.split, q, p->partials(),
-                                   p->stream);
+                                   w.single ? out : nullptr, p->stream);
   });
-  if (st != CS_OK) return st;
+  if (st != CS_OK || w.single) return st;
   return timed_launch(p, CS_PROF_DECODE_MERGE, "decode merge launch", [&] {
     return cs::launch_decode_merge(g, w.convs, w.n_convs, p->partials(), out, p->stream);
   });
@@ -799,9 +804,9 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
       st = timed_launch(p, CS_PROF_MIXED_LAYER, "mixed layer launch", [&] {
         return cs::launch_mixed_layer(g, layer, pw.convs, pw.tiles, pw.n_tiles, q_e(layer), o_e(layer),
                                       dw.convs, dw.n_convs, dw.n_items, dw.split, q_d(layer),
-                                      p->partials(), p->stream);
+                                      p->partials(), dw.single ? o_d(layer) : nullptr, p->stream);
       });
-      if (st == CS_OK)
+      if (st == CS_OK && !dw.single)
         st = timed_launch(p, CS_PROF_DECODE_MERGE, "decode merge launch", [&] {
           return cs::launch_decode_merge(g, dw.convs, dw.n_convs, p->partials(), o_d(layer), p->stream);
         });
@@ -837,7 +842,7 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
     st = span_begin(p, p->stream, CS_PROF_DECODE_SPLIT);
     if (st == CS_OK) st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
       return cs::launch_decode_split(g, 0, dw.convs, dw.n_convs, dw.n_items, dw.split, q_d(0), buf[0],
-                                     p->stream);
+                                     nullptr, p->stream);
     });
     for (int layer = 1; layer < nl && st == CS_OK; ++layer) {
       st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode merge+split launch", [&] {

@@ -118,9 +118,11 @@ __global__ __launch_bounds__(kDecodeItemThreads) void decode_merge_split_kernel(
 
 hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs,
                                int n_convs, int n_items, int split_tokens, const void* q,
-                               float* partials, hipStream_t stream) {
+                               float* partials, void* direct_out, hipStream_t stream) {
   if (n_convs == 0) return hipSuccess;
-  const DecodeArgs a = make_decode_args(g, layer, d_convs, n_convs, n_items, split_tokens, q, nullptr, partials);
+  DecodeArgs a = make_decode_args(g, layer, d_convs, n_convs, n_items, split_tokens, q, direct_out, partials);
+  a.direct = direct_out != nullptr && n_items == n_convs;
+  if (direct_out != nullptr && !a.direct) return hipErrorInvalidValue;
   const int blocks = n_items * g.n_kv_heads;
   if (g.head_dim == 128) decode_split_kernel<128><<<blocks, kDecodeItemThreads, 0, stream>>>(a);
   else if (g.head_dim == 64) decode_split_kernel<64><<<blocks, kDecodeItemThreads, 0, stream>>>(a);

@@ -22,7 +22,8 @@ struct DecodeArgs {
   int n_items;  // work items of the plan (kDecodeSubSplits splits each)
   int split;    // keys per split (per wave), multiple of 32, <= 1024
   const uint16_t* q;
-  uint16_t* out;
+  uint16_t* out;    // with direct: the final output [n_convs][n_q_heads][D]
+  int direct;       // every conversation is one item: write the output instead of a record
   float* partials;  // [n_items * n_kv_heads][group] records of partial_floats(D), one per item
   float scale_log2;
 };
@@ -222,6 +223,14 @@ __device__ __forceinline__ void split_body(const DecodeArgs& a, const int work, 
 #pragma unroll
         for (int r = 0; r < 4; ++r) o[t][r] = __builtin_fmaf(aw, x[16 * t + 4 * qd + r], o[t][r]);
     }
+    if (a.direct) {  // the item is the whole conversation: out = o / l (as the merge computes it)
+      uint16_t* orow = a.out + (static_cast<size_t>(conv_idx) * a.n_kv_heads * a.group + g * a.group + c) * D;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+        st8(orow + 16 * t + 4 * qd, make_uint2(pack_bf16x2(o[t][0] / l, o[t][1] / l),
+                                               pack_bf16x2(o[t][2] / l, o[t][3] / l)));
+      return;
+    }
     // non-temporal: the record is read once, by the merge (about 1% faster than plain stores)
     float* pp = a.partials + (static_cast<size_t>(work) * a.group + c) * partial_floats(D);
 #pragma unroll
@@ -251,6 +260,7 @@ inline DecodeArgs make_decode_args(const PoolGeom& g, int layer, const DecodeCon
   a.q = static_cast<const uint16_t*>(q);
   a.out = static_cast<uint16_t*>(out);
   a.partials = const_cast<float*>(partials);
+  a.direct = 0;
   a.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(g.head_dim)));
   return a;
 }

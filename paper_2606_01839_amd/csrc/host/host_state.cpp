@@ -99,6 +99,7 @@ DecodePlan plan_decode(const std::vector<int32_t>& slots, const std::vector<int6
     start += ns;
   }
   plan.n_items = start;
+  plan.single_item = start == static_cast<int32_t>(lens.size());
   return plan;
 }
 

@@ -92,6 +92,7 @@ constexpr int kDecodeSubSplits = 8;
 struct DecodePlan {
   int32_t split_tokens = 0;  // keys per wave (one split), multiple of 32, <= 1024
   int32_t n_items = 0;       // work items over the batch (per kv head)
+  bool single_item = false;  // every conversation is one work item (no merge of items needed)
   std::vector<DecodeConvDesc> convs;
 };
 

@@ -35,9 +35,11 @@ hipError_t launch_unpack(const PoolGeom& g, const void* wire, const int32_t* d_p
 constexpr int partial_floats(int head_dim) { return head_dim + 4; }
 
 // Decode: split kernel over plan items (partials), then the merge kernel (output).
+// direct_out != nullptr (only when every conversation is one item, n_items == n_convs): the split
+// writes the final output there and no merge follows.
 hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs,
                                int n_convs, int n_items, int split_tokens, const void* q,
-                               float* partials, hipStream_t stream);
+                               float* partials, void* direct_out, hipStream_t stream);
 hipError_t launch_decode_merge(const PoolGeom& g, const DecodeConvDesc* d_convs, int n_convs,
                                const float* partials, void* out, hipStream_t stream);
 // Merge of layer l (merge_partials -> merge_out) and split of layer split_layer (-> split_partials,
@@ -53,7 +55,7 @@ hipError_t launch_mixed_layer(const PoolGeom& g, int layer, const ExtendConvDesc
                               const ExtendTile* d_tiles, int n_tiles, const void* q_ext,
                               void* out_ext, const DecodeConvDesc* d_dec_convs, int n_dec_convs,
                               int n_items, int split_tokens, const void* q_dec, float* partials,
-                              hipStream_t stream);
+                              void* direct_out, hipStream_t stream);
 
 // Query tokens per extend/prefill work tile for this head size and GQA group (the host plan must
 // match).
