@@ -782,9 +782,12 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
   // the extend launches go to a second stream (forked from `stream`, joined back before the call
   // returns), so the matrix-core-bound extend work overlaps the HBM-bound decode work.
   const bool fork = n_ext > 0 && n_dec > 0;
+  // layer order with one launch per layer (extend tiles + decode split) needs no second stream
+  const bool fused_layers = (flags & CS_MIXED_LAYER_ORDERED) && fork && p->desc.head_dim == 128 &&
+                            ew.parts.size() == 1;
   hipStream_t ext_stream = p->stream;
-  if (fork && (st = ensure_side(p)) != CS_OK) return st;
-  if (fork) ext_stream = p->side;
+  if (fork && !fused_layers && (st = ensure_side(p)) != CS_OK) return st;
+  if (fork && !fused_layers) ext_stream = p->side;
   auto fork_side = [&]() -> cs_status {
     CS_HIP(hipEventRecord(p->fork_ev, p->stream), "hipEventRecord");
     CS_HIP(hipStreamWaitEvent(p->side, p->fork_ev, 0), "hipStreamWaitEvent");
@@ -795,7 +798,7 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
     CS_HIP(hipStreamWaitEvent(p->stream, p->join_ev, 0), "hipStreamWaitEvent");
     return CS_OK;
   };
-  if ((flags & CS_MIXED_LAYER_ORDERED) && fork && p->desc.head_dim == 128 && ew.parts.size() == 1) {
+  if (fused_layers) {
     // As in a model forward pass, one layer after the other; each layer is one launch with its
     // extend tiles and its decode split, then the decode merge.
     const cs::PoolGeom g = p->geom();
@@ -834,9 +837,19 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
   for (int layer = 0; layer < nl && n_ext > 0 && st == CS_OK; ++layer)
     st = launch_extend_layer(p, ew, layer, q_e(layer), o_e(layer), ext_stream);
   if (const cs_status se = span_end(p); st == CS_OK) st = se;
-  // Decode of all layers: split(0); then one launch per layer l >= 1 that merges layer l-1 and
-  // splits layer l into the other partial buffer; finally merge(last). One launch per layer.
-  if (n_dec > 0 && st == CS_OK) {
+  // Decode of all layers, one launch per layer: with one work item per conversation each layer's
+  // split writes its output; otherwise split(0), then for l >= 1 a launch that merges layer l-1
+  // and splits layer l into the other partial buffer, and finally merge(last).
+  if (n_dec > 0 && st == CS_OK && dw.single) {
+    const cs::PoolGeom g = p->geom();
+    st = span_begin(p, p->stream, CS_PROF_DECODE_SPLIT);
+    for (int layer = 0; layer < nl && st == CS_OK; ++layer)
+      st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
+        return cs::launch_decode_split(g, layer, dw.convs, dw.n_convs, dw.n_items, dw.split, q_d(layer),
+                                       p->partials(), o_d(layer), p->stream);
+      });
+    if (const cs_status se = span_end(p); st == CS_OK) st = se;
+  } else if (n_dec > 0 && st == CS_OK) {
     const cs::PoolGeom g = p->geom();
     float* buf[2] = {p->partials(), p->partials2()};
     st = span_begin(p, p->stream, CS_PROF_DECODE_SPLIT);

@@ -150,30 +150,31 @@ def test_mixed_step_bitwise_equals_per_layer_calls(n_layers, layer_ordered):
 
 def test_single_item_decode_direct_output_equals_merge_path():
     """A decode batch whose conversations are one work item each (at most 8 splits of 128 keys)
-    has the split kernel write the output directly; the overlapped mixed step always writes
-    partial records and merges them. Both must give the same bits, and match the oracle."""
+    has the split kernel write the output directly; add one long conversation (two items, same
+    128-key splits) and the whole batch goes through partial records and the merge kernel. The
+    short conversations' outputs must be the same bits both ways, and match the oracle."""
     from paper_2606_01839_amd import KVPool
     lens = [1, 17, 300, 777, 1000]
-    mk = lambda: KVPool(1, HQ, HKV, D, n_pages=256, max_convs=8, max_pages_per_conv=64, placement_seed=5)
+    long_len = 1500
+    mk = lambda: KVPool(1, HQ, HKV, D, n_pages=512, max_convs=8, max_pages_per_conv=128, placement_seed=5)
     pa, pb = mk(), mk()
     ha, hb = [], []
-    for c, L in enumerate(lens):
+    for c, L in enumerate(lens + [long_len]):
         k, v = _kv(c, 0, 0, L, "cuda")
         for pool, hs in ((pa, ha), (pb, hb)):
+            if pool is pa and c == len(lens):
+                continue
             h = pool.conv_create()
             pool.kv_append(h, k[None], v[None])
             hs.append(h)
-    k = torch.cat([_kv(c, 0, L, 1)[0] for c, L in enumerate(lens)])[None].contiguous().cuda()
-    v = torch.cat([_kv(c, 0, L, 1)[1] for c, L in enumerate(lens)])[None].contiguous().cuda()
-    q = torch.cat([_q(c, 0, L, 1) for c, L in enumerate(lens)])[None].contiguous().cuda()
-    _, od = pa.mixed_step([], [], ha, k, v, None, q)
-    pb.kv_append_batch(hb, [1] * len(lens), k, v)
-    direct = pb.attn_decode_batch(hb, 0, q[0])
+    q = torch.cat([_q(c, 0, L - 1, 1) for c, L in enumerate(lens + [long_len])]).contiguous().cuda()
+    direct = pa.attn_decode_batch(ha, 0, q[:len(lens)])
+    merged = pb.attn_decode_batch(hb, 0, q)
     torch.cuda.synchronize()
-    assert torch.equal(od[0], direct)
-    for i, (c, L) in enumerate(zip(range(len(lens)), lens)):
-        kk, vv = _kv(c, 0, 0, L + 1)
-        ref = attend_last(sv.bf16_to_f64(q[0, i:i + 1]), sv.bf16_to_f64(kk), sv.bf16_to_f64(vv))
-        assert_close(direct[i:i + 1], ref, f"decode conv {c}")
+    assert torch.equal(direct, merged[:len(lens)])
+    for c, L in enumerate(lens):
+        kk, vv = _kv(c, 0, 0, L)
+        ref = attend_last(sv.bf16_to_f64(q[c:c + 1]), sv.bf16_to_f64(kk), sv.bf16_to_f64(vv))
+        assert_close(direct[c:c + 1], ref, f"decode conv {c}")
     pa.close()
     pb.close()
