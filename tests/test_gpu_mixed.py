@@ -16,15 +16,15 @@ SEED = 5151
 HQ, HKV, D, NL = 32, 8, 128, 2
 
 
-def _kv(conv, layer, start, n, device="cpu"):
-    per = HKV * D
-    k = sv.bf16_tensor(sv.mix_key(SEED, conv, KIND_K, layer), (n, HKV, D), start=start * per, device=device)
-    v = sv.bf16_tensor(sv.mix_key(SEED, conv, KIND_V, layer), (n, HKV, D), start=start * per, device=device)
+def _kv(conv, layer, start, n, device="cpu", hkv=HKV, d=D):
+    per = hkv * d
+    k = sv.bf16_tensor(sv.mix_key(SEED, conv, KIND_K, layer), (n, hkv, d), start=start * per, device=device)
+    v = sv.bf16_tensor(sv.mix_key(SEED, conv, KIND_V, layer), (n, hkv, d), start=start * per, device=device)
     return k, v
 
 
-def _q(conv, layer, start, n, device="cpu"):
-    return sv.bf16_tensor(sv.mix_key(SEED, conv, KIND_Q, layer), (n, HQ, D), start=start * HQ * D,
+def _q(conv, layer, start, n, device="cpu", hq=HQ, d=D):
+    return sv.bf16_tensor(sv.mix_key(SEED, conv, KIND_Q, layer), (n, hq, d), start=start * hq * d,
                           device=device)
 
 
@@ -88,24 +88,26 @@ def test_mixed_step_rejects_overlap_without_changes():
     pool.close()
 
 
+@pytest.mark.parametrize("shape", [(HQ, HKV, D), (4, 2, 64)], ids=["32q8kv_d128", "4q2kv_d64"])
 @pytest.mark.parametrize("layer_ordered", [False, True])
 @pytest.mark.parametrize("n_layers", [1, 3, 4])
-def test_mixed_step_bitwise_equals_per_layer_calls(n_layers, layer_ordered):
+def test_mixed_step_bitwise_equals_per_layer_calls(n_layers, layer_ordered, shape):
     """The mixed step gives bit for bit the outputs of the separate calls (kv_append_batch, then
     attn_extend and attn_decode_batch layer by layer, on a second pool with the same placement),
     both with all layers overlapped (one launch per layer that merges layer l-1 and splits layer l,
-    alternating two partial buffers) and in layer order. Decode-only and extend-only steps
-    included; the last layer's decode outputs are checked against the oracle."""
+    alternating two partial buffers) and in layer order (at d 64 the fork/join form). Decode-only
+    and extend-only steps included; the last layer's decode outputs are checked against the oracle."""
     from paper_2606_01839_amd import KVPool
-    mk = lambda: KVPool(n_layers, HQ, HKV, D, n_pages=900, max_convs=8, max_pages_per_conv=256,
+    hq, hkv, d = shape
+    mk = lambda: KVPool(n_layers, hq, hkv, d, n_pages=900, max_convs=8, max_pages_per_conv=256,
                         placement_seed=77)
     pa, pb = mk(), mk()
     lens0 = [1200, 5, 417, 2049, 96, 800]
     ha, hb, lens = [], [], list(lens0)
 
     def kv_rows(items):
-        ks = [torch.stack([_kv(c, l, s, n)[0] for l in range(n_layers)]) for c, s, n in items]
-        vs = [torch.stack([_kv(c, l, s, n)[1] for l in range(n_layers)]) for c, s, n in items]
+        ks = [torch.stack([_kv(c, l, s, n, hkv=hkv, d=d)[0] for l in range(n_layers)]) for c, s, n in items]
+        vs = [torch.stack([_kv(c, l, s, n, hkv=hkv, d=d)[1] for l in range(n_layers)]) for c, s, n in items]
         return torch.cat(ks, 1).contiguous().cuda(), torch.cat(vs, 1).contiguous().cuda()
 
     for c, L in enumerate(lens0):
@@ -118,9 +120,9 @@ def test_mixed_step_bitwise_equals_per_layer_calls(n_layers, layer_ordered):
     for ext, ext_n, dec in plans:
         items = [(c, lens[c], n) for c, n in zip(ext, ext_n)] + [(c, lens[c], 1) for c in dec]
         k, v = kv_rows(items)
-        qe = (torch.stack([torch.cat([_q(c, l, lens[c], n) for c, n in zip(ext, ext_n)])
+        qe = (torch.stack([torch.cat([_q(c, l, lens[c], n, hq=hq, d=d) for c, n in zip(ext, ext_n)])
                            for l in range(n_layers)]).contiguous().cuda() if ext else None)
-        qd = (torch.stack([torch.cat([_q(c, l, lens[c], 1) for c in dec])
+        qd = (torch.stack([torch.cat([_q(c, l, lens[c], 1, hq=hq, d=d) for c in dec])
                            for l in range(n_layers)]).contiguous().cuda() if dec else None)
         oe, od = pa.mixed_step([ha[c] for c in ext], ext_n, [ha[c] for c in dec], k, v, qe, qd,
                               layer_ordered=layer_ordered)
@@ -138,7 +140,7 @@ def test_mixed_step_bitwise_equals_per_layer_calls(n_layers, layer_ordered):
         if dec:
             layer = n_layers - 1
             for i, c in enumerate(dec):
-                kk, vv = _kv(c, layer, 0, lens[c])
+                kk, vv = _kv(c, layer, 0, lens[c], hkv=hkv, d=d)
                 ref = attend_last(sv.bf16_to_f64(qd[layer, i:i + 1]), sv.bf16_to_f64(kk), sv.bf16_to_f64(vv))
                 assert_close(od[layer, i:i + 1], ref, f"decode conv {c} layer {layer}")
     for c in range(len(lens0)):
