@@ -180,3 +180,48 @@ def test_single_item_decode_direct_output_equals_merge_path():
         assert_close(direct[c:c + 1], ref, f"decode conv {c}")
     pa.close()
     pb.close()
+
+
+@pytest.mark.parametrize("layer_ordered", [False, True])
+def test_mixed_step_single_item_decode_all_layers(layer_ordered):
+    """Short conversations only (one decode work item each): every layer's decode output comes
+    straight from its split launch, in both orders, with and without extend chunks in the step.
+    Outputs equal the per-layer calls bit for bit and match the oracle."""
+    from paper_2606_01839_amd import KVPool
+    nl = 3
+    mk = lambda: KVPool(nl, HQ, HKV, D, n_pages=256, max_convs=8, max_pages_per_conv=64, placement_seed=21)
+    pa, pb = mk(), mk()
+    lens = [3, 40, 250, 600]
+    ha, hb = [], []
+    for c, L in enumerate(lens):
+        k = torch.stack([_kv(c, l, 0, L)[0] for l in range(nl)]).cuda()
+        v = torch.stack([_kv(c, l, 0, L)[1] for l in range(nl)]).cuda()
+        for pool, hs in ((pa, ha), (pb, hb)):
+            h = pool.conv_create()
+            pool.kv_append(h, k, v)
+            hs.append(h)
+    for ext, ext_n, dec in (([], [], [0, 1, 2, 3]), ([3], [20], [0, 1, 2])):
+        items = [(c, lens[c], n) for c, n in zip(ext, ext_n)] + [(c, lens[c], 1) for c in dec]
+        k = torch.cat([torch.stack([_kv(c, l, s, n)[0] for l in range(nl)]) for c, s, n in items], 1)
+        v = torch.cat([torch.stack([_kv(c, l, s, n)[1] for l in range(nl)]) for c, s, n in items], 1)
+        k, v = k.contiguous().cuda(), v.contiguous().cuda()
+        qe = (torch.stack([torch.cat([_q(c, l, lens[c], n) for c, n in zip(ext, ext_n)]) for l in range(nl)])
+              .contiguous().cuda() if ext else None)
+        qd = torch.stack([torch.cat([_q(c, l, lens[c], 1) for c in dec]) for l in range(nl)]).contiguous().cuda()
+        oe, od = pa.mixed_step([ha[c] for c in ext], ext_n, [ha[c] for c in dec], k, v, qe, qd,
+                               layer_ordered=layer_ordered)
+        pb.kv_append_batch([hb[c] for c, _, _ in items], [n for _, _, n in items], k, v)
+        for layer in range(nl):
+            assert torch.equal(od[layer], pb.attn_decode_batch([hb[c] for c in dec], layer, qd[layer]))
+            if ext:
+                assert torch.equal(oe[layer], pb.attn_extend([hb[c] for c in ext], ext_n, layer, qe[layer]))
+        torch.cuda.synchronize()
+        for c, s, n in items:
+            lens[c] = s + n
+        for i, c in enumerate(dec):
+            for layer in (0, nl - 1):
+                kk, vv = _kv(c, layer, 0, lens[c])
+                ref = attend_last(sv.bf16_to_f64(qd[layer, i:i + 1]), sv.bf16_to_f64(kk), sv.bf16_to_f64(vv))
+                assert_close(od[layer, i:i + 1], ref, f"decode conv {c} layer {layer}")
+    pa.close()
+    pb.close()
