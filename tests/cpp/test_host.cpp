@@ -70,6 +70,44 @@ static void decode_plan() {
   CHECK(cs::plan_decode(slots, lens, 8, 49).split_tokens == 512);
 }
 
+// Random batches: the items of a conversation tile [0, len) in splits of split_tokens, 8 per item;
+// item_start is the prefix sum; the split is the largest candidate meeting the target (or 128);
+// single_item holds exactly when every conversation is one item.
+static void decode_plan_random() {
+  std::srand(12345);
+  const int32_t cands[] = {1024, 512, 256, 128};
+  for (int trial = 0; trial < 200; ++trial) {
+    const int n = 1 + std::rand() % 40, hkv = 1 + std::rand() % 8;
+    const int64_t target = 1 + std::rand() % 8000;
+    std::vector<int32_t> slots(n);
+    std::vector<int64_t> lens(n);
+    for (int i = 0; i < n; ++i) {
+      slots[i] = i;
+      lens[i] = 1 + std::rand() % (std::rand() % 2 ? 600 : 40000);
+    }
+    const cs::DecodePlan p = cs::plan_decode(slots, lens, hkv, target);
+    int32_t expect_split = 128;
+    for (int32_t sp : cands) {
+      int64_t waves = 0;
+      for (int64_t L : lens) waves += (L + sp - 1) / sp;
+      if (waves * hkv >= target) { expect_split = sp; break; }
+    }
+    CHECK(p.split_tokens == expect_split);
+    const int64_t ik = static_cast<int64_t>(cs::kDecodeSubSplits) * p.split_tokens;
+    int32_t start = 0;
+    bool single = true;
+    for (int i = 0; i < n; ++i) {
+      CHECK(p.convs[i].slot == slots[i] && p.convs[i].len == lens[i] && p.convs[i].item_start == start);
+      CHECK(p.convs[i].n_splits == (lens[i] + ik - 1) / ik);
+      // the last item of the conversation holds keys, the one after it would not
+      CHECK(static_cast<int64_t>(p.convs[i].n_splits - 1) * ik < lens[i] && p.convs[i].n_splits * ik >= lens[i]);
+      single = single && p.convs[i].n_splits == 1;
+      start += p.convs[i].n_splits;
+    }
+    CHECK(p.n_items == start && p.single_item == single);
+  }
+}
+
 static void extend_plan() {
   std::vector<int32_t> slots = {0, 1};
   std::vector<int64_t> lens = {100, 300};
@@ -135,6 +173,7 @@ int main() {
   pool_basics();
   conv_table();
   decode_plan();
+  decode_plan_random();
   extend_plan();
   append_plan();
   std::puts("host metadata tests passed");
