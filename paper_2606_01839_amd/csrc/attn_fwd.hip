@@ -649,14 +649,15 @@ hipError_t launch_extend(const PoolGeom& g, int layer, const ExtendConvDesc* d_c
 
 hipError_t launch_mixed_layer(const PoolGeom& g, int layer, const ExtendConvDesc* d_ext_convs,
                               const ExtendTile* d_tiles, int n_tiles, const void* q_ext,
-                              void* out_ext, const DecodeConvDesc* d_dec_convs, int n_dec_convs,
-                              int n_items, int split_tokens, const void* q_dec, float* partials,
-                              void* direct_out, hipStream_t stream) {
+                              void* out_ext, const DecodeConvDesc* d_dec_convs,
+                              const int32_t* d_dec_order, int n_dec_convs, int n_items, int split_tokens,
+                              const void* q_dec, float* partials, void* direct_out, hipStream_t stream) {
   if (g.head_dim != 128 || n_tiles == 0 || n_dec_convs == 0) return hipErrorInvalidValue;
+  if (d_dec_order == nullptr || n_items < n_dec_convs) return hipErrorInvalidValue;
   if (direct_out != nullptr && n_items != n_dec_convs) return hipErrorInvalidValue;
   const ExtendArgs ea = make_extend_args(g, layer, d_ext_convs, d_tiles, q_ext, out_ext);
-  DecodeArgs da = make_decode_args(g, layer, d_dec_convs, n_dec_convs, n_items, split_tokens, q_dec,
-                                   direct_out, partials);
+  DecodeArgs da = make_decode_args(g, layer, d_dec_convs, d_dec_order, n_dec_convs, n_items, split_tokens,
+                                   q_dec, direct_out, partials);
   da.direct = direct_out != nullptr;
   const int n_ext = n_tiles * g.n_kv_heads;
   const int blocks = n_ext + n_items * g.n_kv_heads;

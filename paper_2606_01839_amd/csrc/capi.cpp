@@ -400,18 +400,31 @@ cs_status launch_extend_layer(cs_pool* p, const ExtendWork& w, int layer, const 
 
 struct DecodeWork {
   cs::DecodeConvDesc* convs = nullptr;
+  int32_t* order = nullptr;  // launch order of the items
   int n_convs = 0, n_items = 0, split = 0;
   bool single = false;  // one work item per conversation: the split writes the output directly
 };
 
-cs_status upload_decode(cs_pool* p, const std::vector<int32_t>& slots, const std::vector<int64_t>& lens,
-                        DecodeWork* w) {
-  cs::DecodePlan plan = cs::plan_decode(slots, lens, p->desc.n_kv_heads, kDecodeTargetItems);
+cs::DecodePlan plan_decode_batch(const cs_pool* p, const std::vector<int32_t>& slots,
+                                 const std::vector<int64_t>& lens) {
+  return cs::plan_decode(slots, lens, p->desc.n_kv_heads, kDecodeTargetItems);
+}
+
+// Descriptors and launch order of a decode plan, as uploaded back to back.
+size_t decode_upload_bytes(const cs::DecodePlan& plan) {
+  return align_up(plan.convs.size() * sizeof(cs::DecodeConvDesc), 16) + plan.order.size() * sizeof(int32_t);
+}
+
+cs_status check_decode_plan(const cs_pool* p, const cs::DecodePlan& plan) {
   if (plan.n_items > max_decode_items(p->desc)) return fail(CS_ENOMEM, "decode partials exceed the workspace");
-  void* d = nullptr;
-  cs_status st = upload(p, plan.convs.data(), plan.convs.size() * sizeof(cs::DecodeConvDesc), &d);
+  if (decode_upload_bytes(plan) > kQuarter) return fail(CS_ENOMEM, "batch descriptor exceeds the metadata ring");
+  return CS_OK;
+}
+
+cs_status upload_decode(cs_pool* p, const cs::DecodePlan& plan, DecodeWork* w) {
+  cs_status st = check_decode_plan(p, plan);
   if (st != CS_OK) return st;
-  w->convs = static_cast<cs::DecodeConvDesc*>(d);
+  if ((st = upload2(p, plan.convs, plan.order, &w->convs, &w->order)) != CS_OK) return st;
   w->n_convs = static_cast<int>(plan.convs.size());
   w->n_items = plan.n_items;
   w->split = plan.split_tokens;
@@ -423,7 +436,7 @@ cs_status upload_decode(cs_pool* p, const std::vector<int32_t>& slots, const std
 cs_status launch_decode_layer(cs_pool* p, const DecodeWork& w, int layer, const void* q, void* out) {
   const cs::PoolGeom g = p->geom();
   cs_status st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
-    return cs::launch_decode_split(g, layer, w.convs, w.n_convs, w.n_items, w.split, q, p->partials(),
+    return cs::launch_decode_split(g, layer, w.convs, w.order, w.n_convs, w.n_items, w.split, q, p->partials(),
                                    w.single ? out : nullptr, p->stream);
   });
   if (st != CS_OK || w.single) return st;
@@ -660,7 +673,7 @@ cs_status cs_attn_decode_batch(cs_pool* p, int32_t n, const cs_conv* convs, int3
     lens[i] = cv[i]->len;
   }
   DecodeWork w;
-  if ((st = upload_decode(p, slots, lens, &w)) != CS_OK) return st;
+  if ((st = upload_decode(p, plan_decode_batch(p, slots, lens), &w)) != CS_OK) return st;
   return launch_decode_layer(p, w, layer, q, out);
 }
 
@@ -750,26 +763,34 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
   if ((ext_rows > 0 && (!q_ext || !out_ext)) || (n_dec > 0 && (!q_dec || !out_dec)))
     return fail(CS_EINVAL, "null q/out");
   if (align_up(static_cast<size_t>(n_ext) * sizeof(cs::ExtendConvDesc), 16) + kAlign +
-              sizeof(cs::ExtendTile) > kQuarter ||
-      static_cast<size_t>(n_dec) * sizeof(cs::DecodeConvDesc) > kQuarter)
+          sizeof(cs::ExtendTile) > kQuarter)
     return fail(CS_ENOMEM, "batch descriptor exceeds the metadata ring");
+  // The decode plan covers each decoding conversation with its new token; it is checked before
+  // the append so that a batch it cannot take leaves the pool unchanged.
+  std::vector<int32_t> d_slots(n_dec);
+  std::vector<int64_t> d_lens(n_dec);
+  for (int32_t i = 0; i < n_dec; ++i) {
+    d_slots[i] = cs::ConvTable::slot_of(dec_convs[i]);
+    d_lens[i] = cv[n_ext + i]->len + 1;
+  }
+  cs::DecodePlan d_plan;
+  if (n_dec > 0) {
+    d_plan = plan_decode_batch(p, d_slots, d_lens);
+    if ((st = check_decode_plan(p, d_plan)) != CS_OK) return st;
+  }
   // append every new token (all layers); validates capacity and commits the host metadata
   if ((st = append_impl(p, static_cast<int32_t>(all.size()), all.data(), n_new.data(), k, v, stream)) != CS_OK)
     return st;
-  std::vector<int32_t> e_slots(n_ext), d_slots(n_dec), e_q(n_new.begin(), n_new.begin() + n_ext);
-  std::vector<int64_t> e_lens(n_ext), d_lens(n_dec);
+  std::vector<int32_t> e_slots(n_ext), e_q(n_new.begin(), n_new.begin() + n_ext);
+  std::vector<int64_t> e_lens(n_ext);
   for (int32_t i = 0; i < n_ext; ++i) {
     e_slots[i] = cs::ConvTable::slot_of(ext_convs[i]);
     e_lens[i] = p->convs.find(ext_convs[i])->len;
   }
-  for (int32_t i = 0; i < n_dec; ++i) {
-    d_slots[i] = cs::ConvTable::slot_of(dec_convs[i]);
-    d_lens[i] = p->convs.find(dec_convs[i])->len;
-  }
   ExtendWork ew;
   DecodeWork dw;
   if (n_ext > 0 && (st = upload_extend(p, e_slots, e_lens, e_q, &ew)) != CS_OK) return st;
-  if (n_dec > 0 && (st = upload_decode(p, d_slots, d_lens, &dw)) != CS_OK) return st;
+  if (n_dec > 0 && (st = upload_decode(p, d_plan, &dw)) != CS_OK) return st;
   const size_t row_bytes = static_cast<size_t>(p->desc.n_q_heads) * p->desc.head_dim * 2;
   const int nl = p->desc.n_layers;
   const size_t ext_layer_bytes = static_cast<size_t>(ext_rows) * row_bytes;
@@ -806,7 +827,7 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
     for (int layer = 0; layer < nl && st == CS_OK; ++layer) {
       st = timed_launch(p, CS_PROF_MIXED_LAYER, "mixed layer launch", [&] {
         return cs::launch_mixed_layer(g, layer, pw.convs, pw.tiles, pw.n_tiles, q_e(layer), o_e(layer),
-                                      dw.convs, dw.n_convs, dw.n_items, dw.split, q_d(layer),
+                                      dw.convs, dw.order, dw.n_convs, dw.n_items, dw.split, q_d(layer),
                                       p->partials(), dw.single ? o_d(layer) : nullptr, p->stream);
       });
       if (st == CS_OK && !dw.single)
@@ -845,7 +866,7 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
     st = span_begin(p, p->stream, CS_PROF_DECODE_SPLIT);
     for (int layer = 0; layer < nl && st == CS_OK; ++layer)
       st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
-        return cs::launch_decode_split(g, layer, dw.convs, dw.n_convs, dw.n_items, dw.split, q_d(layer),
+        return cs::launch_decode_split(g, layer, dw.convs, dw.order, dw.n_convs, dw.n_items, dw.split, q_d(layer),
                                        p->partials(), o_d(layer), p->stream);
       });
     if (const cs_status se = span_end(p); st == CS_OK) st = se;
@@ -854,12 +875,12 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
     float* buf[2] = {p->partials(), p->partials2()};
     st = span_begin(p, p->stream, CS_PROF_DECODE_SPLIT);
     if (st == CS_OK) st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode split launch", [&] {
-      return cs::launch_decode_split(g, 0, dw.convs, dw.n_convs, dw.n_items, dw.split, q_d(0), buf[0],
+      return cs::launch_decode_split(g, 0, dw.convs, dw.order, dw.n_convs, dw.n_items, dw.split, q_d(0), buf[0],
                                      nullptr, p->stream);
     });
     for (int layer = 1; layer < nl && st == CS_OK; ++layer) {
       st = timed_launch(p, CS_PROF_DECODE_SPLIT, "decode merge+split launch", [&] {
-        return cs::launch_decode_merge_split(g, layer, dw.convs, dw.n_convs, dw.n_items, dw.split,
+        return cs::launch_decode_merge_split(g, layer, dw.convs, dw.order, dw.n_convs, dw.n_items, dw.split,
                                              q_d(layer), buf[layer % 2], buf[(layer - 1) % 2],
                                              o_d(layer - 1), p->stream);
       });

@@ -117,10 +117,12 @@ __global__ __launch_bounds__(kDecodeItemThreads) void decode_merge_split_kernel(
 }
 
 hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs,
-                               int n_convs, int n_items, int split_tokens, const void* q,
-                               float* partials, void* direct_out, hipStream_t stream) {
+                               const int32_t* d_order, int n_convs, int n_items, int split_tokens,
+                               const void* q, float* partials, void* direct_out, hipStream_t stream) {
   if (n_convs == 0) return hipSuccess;
-  DecodeArgs a = make_decode_args(g, layer, d_convs, n_convs, n_items, split_tokens, q, direct_out, partials);
+  if (d_order == nullptr || n_items < n_convs) return hipErrorInvalidValue;
+  DecodeArgs a = make_decode_args(g, layer, d_convs, d_order, n_convs, n_items, split_tokens, q, direct_out,
+                                  partials);
   a.direct = direct_out != nullptr && n_items == n_convs;
   if (direct_out != nullptr && !a.direct) return hipErrorInvalidValue;
   const int blocks = n_items * g.n_kv_heads;
@@ -131,13 +133,15 @@ hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDes
 }
 
 hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const DecodeConvDesc* d_convs,
-                                     int n_convs, int n_items, int split_tokens, const void* q,
-                                     float* split_partials, const float* merge_partials,
+                                     const int32_t* d_order, int n_convs, int n_items, int split_tokens,
+                                     const void* q, float* split_partials, const float* merge_partials,
                                      void* merge_out, hipStream_t stream) {
   if (n_convs == 0) return hipSuccess;
-  const DecodeArgs as = make_decode_args(g, split_layer, d_convs, n_convs, n_items, split_tokens, q, nullptr,
-                                  split_partials);
-  const DecodeArgs am = make_decode_args(g, 0, d_convs, n_convs, 0, 0, nullptr, merge_out, merge_partials);
+  if (d_order == nullptr || n_items < n_convs) return hipErrorInvalidValue;
+  const DecodeArgs as = make_decode_args(g, split_layer, d_convs, d_order, n_convs, n_items, split_tokens, q,
+                                         nullptr, split_partials);
+  const DecodeArgs am = make_decode_args(g, 0, d_convs, nullptr, n_convs, 0, 0, nullptr, merge_out,
+                                         merge_partials);
   constexpr int kPerBlock = kDecodeItemThreads / 256;
   const int merge_blocks = (n_convs * g.n_q_heads + kPerBlock - 1) / kPerBlock;
   const int blocks = merge_blocks + n_items * g.n_kv_heads;
@@ -152,7 +156,7 @@ hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const D
 hipError_t launch_decode_merge(const PoolGeom& g, const DecodeConvDesc* d_convs, int n_convs,
                                const float* partials, void* out, hipStream_t stream) {
   if (n_convs == 0) return hipSuccess;
-  const DecodeArgs a = make_decode_args(g, 0, d_convs, n_convs, 0, 0, nullptr, out, partials);
+  const DecodeArgs a = make_decode_args(g, 0, d_convs, nullptr, n_convs, 0, 0, nullptr, out, partials);
   const dim3 grid(n_convs, g.n_q_heads);
   if (g.head_dim == 128) decode_merge_kernel<128><<<grid, 256, 0, stream>>>(a);
   else if (g.head_dim == 64) decode_merge_kernel<64><<<grid, 256, 0, stream>>>(a);

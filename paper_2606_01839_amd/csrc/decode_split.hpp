@@ -26,6 +26,7 @@ struct DecodeArgs {
   int direct;       // every conversation is one item: write the output instead of a record
   float* partials;  // [n_items * n_kv_heads][group] records of partial_floats(D), one per item
   float scale_log2;
+  const int32_t* order;  // [n_items]: workgroup w takes item order[w / n_kv_heads]
 };
 
 // Kernel arguments read by every wave alike are loaded through the constant address space, so
@@ -62,14 +63,16 @@ constexpr int kDecodeItemThreads = 64 * kDecodeSubSplits;
 template <int D>
 constexpr int split_exchange_floats() { return (kDecodeSubSplits - 1) * 8 * (D + 2); }
 
-// Work item `work` = (item, kv head) of the plan, taken by one workgroup of kDecodeSubSplits waves
-// (this wave = `wave`; `xch` = its LDS exchange area, split_exchange_floats<D>() floats). Wave w
-// reads split w of the item -- keys [k0 + w split, k0 + (w + 1) split) -- once; then the other
-// waves hand their (o, m, l) to wave 0 through LDS, which merges them in the order w = 0, 1, ...
-// and writes the item's one partial record: far fewer, larger writes interleaved with the KV
-// stream than one record per wave (the HBM reads run 7% faster with 8 waves per item than with
-// one). Every wave reaches the one barrier, also in a workgroup whose work unit lies past the end
-// (work >= n_items * n_kv_heads: no keys, nothing written).
+// Work unit `work` = (order[work / n_kv_heads], work % n_kv_heads) = (item, kv head) of the plan,
+// taken by one workgroup of kDecodeSubSplits waves (this wave = `wave`; `xch` = its LDS exchange
+// area, split_exchange_floats<D>() floats). The item's n keys are shared out evenly: wave w reads
+// keys [k0 + w s, k0 + (w + 1) s) with s = ceil(n / kDecodeSubSplits) rounded up to a page pair,
+// so a short last item keeps all its waves busy for a short time instead of a few of them for a
+// full split. Then the other waves hand their (o, m, l) to wave 0 through LDS, which merges them
+// in the order w = 0, 1, ... and writes the item's one partial record: far fewer, larger writes
+// interleaved with the KV stream than one record per wave (the HBM reads run 7% faster with 8
+// waves per item than with one). Every wave reaches the one barrier, also in a workgroup whose
+// work unit lies past the end (work >= n_items * n_kv_heads: no keys, nothing written).
 template <int D>
 __device__ __forceinline__ void split_body(const DecodeArgs& a, const int work, const int wave,
                                            float* xch) {
@@ -77,12 +80,16 @@ __device__ __forceinline__ void split_body(const DecodeArgs& a, const int work, 
   constexpr int DT = D / 16;  // 16-dim tiles of the output
   const int lane = threadIdx.x & 63;
   const bool valid = work < a.n_items * a.n_kv_heads;
-  const int item = valid ? work / a.n_kv_heads : 0, g = work % a.n_kv_heads;
+  const int item = as_const(a.order)[valid ? work / a.n_kv_heads : 0], g = work % a.n_kv_heads;
   const auto* convs = as_const(a.convs);
   const int conv_idx = find_conv(convs, a.n_convs, item);
   const DecodeConvDesc cd = load_desc(convs + conv_idx);
-  const int k_begin = ((item - cd.item_start) * kDecodeSubSplits + wave) * a.split;
-  const int k_end = valid ? min(cd.len, k_begin + a.split) : k_begin;
+  const int item_k0 = (item - cd.item_start) * kDecodeSubSplits * a.split;
+  const int item_k1 = min(cd.len, item_k0 + kDecodeSubSplits * a.split);
+  const int wave_keys = ((item_k1 - item_k0 + kDecodeSubSplits - 1) / kDecodeSubSplits + 2 * kPageTokens - 1) &
+                        ~(2 * kPageTokens - 1);  // <= split (a multiple of 32)
+  const int k_begin = item_k0 + wave * wave_keys;
+  const int k_end = valid ? min(item_k1, k_begin + wave_keys) : k_begin;
   const int n_pg = k_end > k_begin ? (k_end - k_begin + kPageTokens - 1) / kPageTokens : 0;
   const int32_t* pt = a.page_table + static_cast<size_t>(cd.slot) * a.max_pages + k_begin / kPageTokens;
 
@@ -232,7 +239,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs& a, const int work, 
       return;
     }
     // non-temporal: the record is read once, by the merge (about 1% faster than plain stores)
-    float* pp = a.partials + (static_cast<size_t>(work) * a.group + c) * partial_floats(D);
+    float* pp = a.partials + ((static_cast<size_t>(item) * a.n_kv_heads + g) * a.group + c) * partial_floats(D);
 #pragma unroll
     for (int t = 0; t < DT; ++t) __builtin_nontemporal_store(o[t], reinterpret_cast<f32x4*>(pp + 16 * t + 4 * qd));
     if (qd == 0) {
@@ -242,9 +249,9 @@ __device__ __forceinline__ void split_body(const DecodeArgs& a, const int work, 
   }
 }
 
-inline DecodeArgs make_decode_args(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs, int n_convs,
-                            int n_items, int split_tokens, const void* q, void* out,
-                            const float* partials) {
+inline DecodeArgs make_decode_args(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs,
+                                   const int32_t* d_order, int n_convs, int n_items, int split_tokens,
+                                   const void* q, void* out, const float* partials) {
   DecodeArgs a;
   a.pool = static_cast<const uint16_t*>(g.pool);
   a.n_pages = g.n_pages;
@@ -254,6 +261,7 @@ inline DecodeArgs make_decode_args(const PoolGeom& g, int layer, const DecodeCon
   a.page_table = g.page_table;
   a.max_pages = g.max_pages;
   a.convs = d_convs;
+  a.order = d_order;
   a.n_convs = n_convs;
   a.n_items = n_items;
   a.split = split_tokens;

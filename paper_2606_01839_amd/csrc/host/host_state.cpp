@@ -100,6 +100,13 @@ DecodePlan plan_decode(const std::vector<int32_t>& slots, const std::vector<int6
   }
   plan.n_items = start;
   plan.single_item = start == static_cast<int32_t>(lens.size());
+  std::vector<int64_t> keys(static_cast<size_t>(start));
+  for (const DecodeConvDesc& c : plan.convs)
+    for (int32_t s = 0; s < c.n_splits; ++s) keys[c.item_start + s] = std::min<int64_t>(item_keys, c.len - s * item_keys);
+  plan.order.resize(static_cast<size_t>(start));
+  std::iota(plan.order.begin(), plan.order.end(), 0);
+  std::stable_sort(plan.order.begin(), plan.order.end(),
+                   [&](int32_t x, int32_t y) { return keys[x] > keys[y]; });
   return plan;
 }
 

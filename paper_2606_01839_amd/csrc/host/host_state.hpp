@@ -76,8 +76,9 @@ class ConvTable {
 // Work plans (plain structs uploaded to the device as-is; layouts shared with the kernels).
 // ---------------------------------------------------------------------------------------------
 
-// Decode: one work item = (conversation b, logical split s, kv head); a split covers keys
-// [s*split, min(len, (s+1)*split)). Items of conversation b are numbered item_start[b] + s.
+// Decode: one work item = (conversation b, item s, kv head) covers keys [s*K, min(len, (s+1)*K))
+// with K = kDecodeSubSplits * split_tokens, shared out evenly over its waves in whole page pairs.
+// Items of conversation b are numbered item_start[b] + s.
 struct DecodeConvDesc {
   int32_t slot;        // row of the device page-table mirror
   int32_t len;         // tokens
@@ -94,6 +95,10 @@ struct DecodePlan {
   int32_t n_items = 0;       // work items over the batch (per kv head)
   bool single_item = false;  // every conversation is one work item (no merge of items needed)
   std::vector<DecodeConvDesc> convs;
+  // Launch order: workgroup w takes item order[w / n_kv_heads]. Full items (K keys) come first, in
+  // conversation order, then the shorter last items by decreasing key count, so the last round
+  // of workgroups on the chip holds the shortest ones.
+  std::vector<int32_t> order;
 };
 
 // Choose the split size: the largest candidate for which the splits holding keys, over all kv

@@ -34,18 +34,19 @@ hipError_t launch_unpack(const PoolGeom& g, const void* wire, const int32_t* d_p
 // floats, so records stay 16-byte aligned.
 constexpr int partial_floats(int head_dim) { return head_dim + 4; }
 
-// Decode: split kernel over plan items (partials), then the merge kernel (output).
+// Decode: split kernel over plan items (partials), then the merge kernel (output). d_order: the
+// plan's launch order of its n_items items (a permutation).
 // direct_out != nullptr (only when every conversation is one item, n_items == n_convs): the split
 // writes the final output there and no merge follows.
 hipError_t launch_decode_split(const PoolGeom& g, int layer, const DecodeConvDesc* d_convs,
-                               int n_convs, int n_items, int split_tokens, const void* q,
+                               const int32_t* d_order, int n_convs, int n_items, int split_tokens, const void* q,
                                float* partials, void* direct_out, hipStream_t stream);
 hipError_t launch_decode_merge(const PoolGeom& g, const DecodeConvDesc* d_convs, int n_convs,
                                const float* partials, void* out, hipStream_t stream);
 // Merge of layer l (merge_partials -> merge_out) and split of layer split_layer (-> split_partials,
 // a different buffer) in one launch; the same conversations and plan for both.
 hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const DecodeConvDesc* d_convs,
-                                     int n_convs, int n_items, int split_tokens, const void* q,
+                                     const int32_t* d_order, int n_convs, int n_items, int split_tokens, const void* q,
                                      float* split_partials, const float* merge_partials,
                                      void* merge_out, hipStream_t stream);
 
@@ -53,7 +54,8 @@ hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const D
 // its decode split (partials; the merge follows as launch_decode_merge).
 hipError_t launch_mixed_layer(const PoolGeom& g, int layer, const ExtendConvDesc* d_ext_convs,
                               const ExtendTile* d_tiles, int n_tiles, const void* q_ext,
-                              void* out_ext, const DecodeConvDesc* d_dec_convs, int n_dec_convs,
+                              void* out_ext, const DecodeConvDesc* d_dec_convs,
+                              const int32_t* d_dec_order, int n_dec_convs,
                               int n_items, int split_tokens, const void* q_dec, float* partials,
                               void* direct_out, hipStream_t stream);
 

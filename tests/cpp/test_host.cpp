@@ -63,6 +63,8 @@ static void decode_plan() {
   const int32_t n1 = static_cast<int32_t>((1000 + ik - 1) / ik), n2 = static_cast<int32_t>((4096 + ik - 1) / ik);
   CHECK(p.convs.size() == 3 && p.convs[0].n_splits == 1 && p.convs[1].n_splits == n1 && p.convs[2].n_splits == n2);
   CHECK(p.convs[1].item_start == 1 && p.convs[2].item_start == 1 + n1 && p.n_items == 1 + n1 + n2);
+  // launch order: the full items (conversation 2's four) first, then 1000 keys, then 1 key
+  CHECK(n1 == 1 && n2 == 4 && (p.order == std::vector<int32_t>{2, 3, 4, 5, 1, 0}));
   cs::DecodePlan q = cs::plan_decode(slots, lens, 8, 1);  // any split satisfies -> largest
   CHECK(q.split_tokens == 1024 && q.n_items == 3);         // one item each (4096 <= 4 * 1024)
   // the target counts splits holding keys: 1 + 1 + 4 = 6 splits of 1024 keys, x 8 kv heads = 48
@@ -72,7 +74,9 @@ static void decode_plan() {
 
 // Random batches: the items of a conversation tile [0, len) in splits of split_tokens, 8 per item;
 // item_start is the prefix sum; the split is the largest candidate meeting the target (or 128);
-// single_item holds exactly when every conversation is one item.
+// single_item holds exactly when every conversation is one item; the launch order is a
+// permutation of the items: every full item, in item order, then the others by decreasing key
+// count (ties in item order).
 static void decode_plan_random() {
   std::srand(12345);
   const int32_t cands[] = {1024, 512, 256, 128};
@@ -105,6 +109,21 @@ static void decode_plan_random() {
       start += p.convs[i].n_splits;
     }
     CHECK(p.n_items == start && p.single_item == single);
+    std::vector<int64_t> keys;
+    for (int i = 0; i < n; ++i)
+      for (int s = 0; s < p.convs[i].n_splits; ++s) keys.push_back(std::min<int64_t>(ik, lens[i] - s * ik));
+    CHECK(p.order.size() == keys.size());
+    std::vector<char> seen(keys.size(), 0);
+    for (size_t j = 0; j < p.order.size(); ++j) {
+      const int32_t it = p.order[j];
+      CHECK(it >= 0 && it < p.n_items && !seen[it]);
+      seen[it] = 1;
+      if (j > 0) {
+        const int32_t prev = p.order[j - 1];
+        CHECK(keys[prev] >= keys[it]);
+        if (keys[prev] == keys[it]) CHECK(prev < it);
+      }
+    }
   }
 }
 
