@@ -1,8 +1,9 @@
 // Batched single-token decode attention over paged KV (split-K "flash decoding").
 //
-// One wave reads one split (`split` consecutive keys) of one (conversation, kv head) once and
-// serves all G query heads of the kv head; a work item is kDecodeSubSplits consecutive splits, one
-// workgroup. The two contractions per page pair are done on the matrix cores with
+// A work item is up to kDecodeSubSplits splits (`split` keys each) of consecutive keys of one
+// (conversation, kv head), taken by one workgroup; its waves share its keys evenly, each reading
+// its range once and serving all G query heads of the kv head. Workgroups take the items in the
+// plan's launch order (full items first, then shorter ones). The two contractions per page pair are done on the matrix cores with
 // v_mfma_f32_16x16x32_bf16, the GQA group as the 16-wide N side:
 //   S^T[key][head] = K[key][:] . Q[head][:]          (A = K rows straight from the page,
 //                                                     B = Q, 8 consecutive dims per lane)
