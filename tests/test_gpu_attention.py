@@ -145,6 +145,27 @@ def test_decode_bitwise_deterministic_and_placement_invariant():
     assert torch.equal(a, c), "decode depends on physical page placement"
 
 
+def test_decode_bitwise_independent_of_batch_order():
+    """Work items are launched in an order that depends on the whole batch (full items first, then
+    the others by decreasing key count); a conversation's output must not: the same conversations
+    decoded in reversed and shuffled batch order give bitwise the same rows."""
+    hq, hkv, d = 32, 8, 128
+    lens = [5, 700, 1500, 2600, 1024, 1025, 3000, 2048]
+    pool = _pool(hq, hkv, d, sum((L + 15) // 16 for L in lens) + 8, seed=5)
+    convs = []
+    for i, L in enumerate(lens):
+        c = pool.conv_create()
+        _fill(pool, c, i, L, hkv, d)
+        convs.append(c)
+    q = torch.cat([q_tokens(SEED, i, 0, L - 1, 1, hq, d) for i, L in enumerate(lens)]).cuda()
+    base = pool.attn_decode_batch(convs, 0, q)
+    for perm in (list(reversed(range(len(lens)))), [3, 0, 6, 1, 7, 2, 5, 4]):
+        out = pool.attn_decode_batch([convs[j] for j in perm], 0, q[perm].contiguous())
+        torch.cuda.synchronize()
+        assert torch.equal(out, base[perm]), perm
+    pool.close()
+
+
 def test_extend_bitwise_placement_invariant():
     a = _extend_case(32, 8, 128, [0, 500], [200, 150], pool_seed=1)
     b = _extend_case(32, 8, 128, [0, 500], [200, 150], pool_seed=777)
