@@ -29,15 +29,26 @@ def kv_head_of(h: int, n_q_heads: int, n_kv_heads: int) -> int:
     return h // (n_q_heads // n_kv_heads)
 
 
-def probabilities(q: np.ndarray, k: np.ndarray, pos: int) -> np.ndarray:
-    """Softmax weights of one query row over keys 0..pos.
+def weights(q_rows: np.ndarray, pos, k_head: np.ndarray) -> np.ndarray:
+    """Softmax weights of query rows of one head over the keys of its KV head (steps 1-2 below).
 
-    q: [d] float64; k: [>= pos+1][d] float64 (one KV head). Returns [pos+1] float64.
+    q_rows: [r][d] float64 query rows; pos: [r] absolute positions; k_head: [>= max(pos)+1][d]
+    float64 keys of the row's KV head. Returns [r][max(pos)+1] float64: row i holds
+    softmax_j(q_i . k_j / sqrt(d)) over the visible keys j <= pos[i] and exact zeros for the keys
+    past pos[i] (the causal mask). The maximum is subtracted before exponentiating (a stable
+    softmax; the result is mathematically the same).
     """
-    d = q.shape[-1]
-    s = (k[: pos + 1] @ q) / math.sqrt(d)
-    w = np.exp(s - s.max())
-    return w / w.sum()
+    q_rows = np.asarray(q_rows, dtype=np.float64)
+    pos = np.asarray(pos, dtype=np.int64).reshape(-1)
+    d = q_rows.shape[-1]
+    nk = int(pos.max()) + 1
+    s = (q_rows @ k_head[:nk].T) * (1.0 / math.sqrt(d))               # step 1: scores
+    visible = np.arange(nk)[None, :] <= pos[:, None]
+    s = np.where(visible, s, -np.inf)
+    m = s.max(axis=1, keepdims=True)                                    # step 2: stable softmax
+    w = np.exp(s - m)
+    z = w.sum(axis=1, keepdims=True)
+    return w / z
 
 
 def attend_rows(q: np.ndarray, pos, k: np.ndarray, v: np.ndarray, block: int = 256) -> np.ndarray:
@@ -62,20 +73,12 @@ def attend_rows(q: np.ndarray, pos, k: np.ndarray, v: np.ndarray, block: int = 2
     assert hq % hkv == 0 and k.shape[2] == d and v.shape == k.shape
     assert pos.shape[0] == r and pos.min() >= 0 and pos.max() < k.shape[0]
     out = np.empty((r, hq, d), dtype=np.float64)
-    inv_sqrt_d = 1.0 / math.sqrt(d)
     for h in range(hq):
         g = kv_head_of(h, hq, hkv)
         for b0 in range(0, r, block):
             rows = slice(b0, min(r, b0 + block))
-            p = pos[rows]
-            nk = int(p.max()) + 1
-            s = (q[rows, h, :] @ k[:nk, g, :].T) * inv_sqrt_d           # step 1: scores
-            visible = np.arange(nk)[None, :] <= p[:, None]
-            s = np.where(visible, s, -np.inf)
-            m = s.max(axis=1, keepdims=True)                             # step 2: stable softmax
-            w = np.exp(s - m)
-            z = w.sum(axis=1, keepdims=True)
-            out[rows, h, :] = (w / z) @ v[:nk, g, :]                     # step 3: weighted values
+            w = weights(q[rows, h, :], pos[rows], k[:, g, :])
+            out[rows, h, :] = w @ v[: w.shape[1], g, :]                  # step 3: weighted values
     return out
 
 

@@ -4,13 +4,14 @@ reactive scheduler (arxiv 2606.01839, Section 4), written out plainly in Python.
 Test infrastructure only: tests/ and bench.py's CPU baseline may import it; the library never
 does. It shares no code with the C++ scheduler (paper_2606_01839_amd/csrc/host/sched.cpp).
 
+- curve_eval: the fitted latency t(L) = c0 + c1 L + c2 L^2.
 - prefill_curve_fit: least squares t = c0 + c1 L + c2 L^2 over measured (L, t) samples (Section
   3.1 profiles the prefill latency offline and finds it quadratic in the input length), using
   numpy's least-squares solver on the design matrix [1, x, x^2] of x = L / max|L|.
 - provision: Section 4.1. The prefiller saturates at R* = T_p / L_in conversations per second;
   N decoders must satisfy N * T_d >= R * L_d (throughput) and N * B >= R * W (memory) at R = R*;
-  N is the smallest integer greater than both bounds (reading: "an integer more than satisfying
-  both inequalities").
+  N is the smallest integer strictly above both bounds, N = floor(max(bounds)) + 1 (the reading
+  adopted for Section 4.1's rule that N exceeds what both inequalities require).
 - bind: Section 4.2. A transferred conversation is bound to the decoder with the lowest current
   KV-cache occupancy; readings: occupancy is the fraction of a decoder's pages held by live
   conversations, only decoders with enough free pages for the conversation are candidates, ties go

@@ -14,7 +14,7 @@ import os
 import numpy as np
 import pytest
 
-from oracle.attention import attend_last, attend_rows, probabilities, kv_head_of
+from oracle.attention import attend_last, attend_rows, kv_head_of, weights
 from oracle import kvwire
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -118,13 +118,68 @@ def test_concentration_on_aligned_key():
         np.testing.assert_allclose(got[0, 0], v[jstar, 0], atol=1e-8)
 
 
-def test_probabilities_sum_to_one():
+def brute_weights(q_row, pos, k_head):
+    """Pure-Python softmax(q . k_j / sqrt(d)) over keys 0..pos, zeros after: independent of the oracle."""
+    d = len(q_row)
+    s = [math.fsum(q_row[e] * k_head[j][e] for e in range(d)) / math.sqrt(d) for j in range(pos + 1)]
+    m = max(s)
+    e = [math.exp(x - m) for x in s]
+    z = math.fsum(e)
+    return [x / z for x in e]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_weights_match_brute_force_softmax(seed):
+    """The weights attend_rows forms, scale 1/sqrt(d) included, against a brute-force softmax."""
+    rng = np.random.default_rng(100 + seed)
+    d = [4, 16, 64][seed % 3]
+    L = int(rng.integers(1, 30))
+    k = rng.standard_normal((L, d)) * 2.0
+    pos = rng.integers(0, L, size=5)
+    q = rng.standard_normal((5, d)) * 2.0
+    w = weights(q, pos, k)
+    assert w.shape == (5, int(pos.max()) + 1)
+    for i in range(5):
+        ref = brute_weights(q[i].tolist(), int(pos[i]), k.tolist())
+        np.testing.assert_allclose(w[i, : pos[i] + 1], ref, rtol=1e-12, atol=1e-300)
+        assert (w[i, pos[i] + 1:] == 0).all()                 # keys past the row are masked exactly
+
+
+def test_weights_rows_scaled_far_apart():
+    """A stable softmax per row: one row's scores near 0, another's in the thousands."""
+    rng = np.random.default_rng(21)
+    k = rng.standard_normal((6, 4)) * 3
+    q = np.stack([rng.standard_normal(4), 200 * k[5]])     # second row: score 100 |k5|^2 >> 745
+    w = weights(q, [5, 5], k)
+    for i in range(2):
+        np.testing.assert_allclose(w[i], brute_weights(q[i].tolist(), 5, k.tolist()), rtol=1e-12, atol=0)
+
+
+def test_weights_hand_worked_example():
+    """d = 4 (scale 1/2): q = (2 ln 2, 2 ln 3, 0, 0) against k0 = 0, k1 = e0, k2 = e1 scores
+    (0, ln 2, ln 3), so the weights are (1, 2, 3) / 6 at position 2 and (1, 2) / 3 at position 1."""
+    k = np.array([[0, 0, 0, 0], [1, 0, 0, 0], [0, 1, 0, 0]], dtype=np.float64)
+    q = np.array([[2 * math.log(2), 2 * math.log(3), 0, 0]] * 2)
+    w = weights(q, [2, 1], k)
+    np.testing.assert_allclose(w, [[1 / 6, 2 / 6, 3 / 6], [1 / 3, 2 / 3, 0.0]], rtol=0, atol=1e-15)
+
+
+def test_weights_rows_sum_to_one_and_give_attend_rows():
+    """Every weight row of attend_rows' own softmax sums to 1, and weights @ V is its output."""
     rng = np.random.default_rng(5)
-    k = rng.standard_normal((50, 32)) * 4
-    for p in (0, 1, 17, 49):
-        w = probabilities(rng.standard_normal(32) * 4, k, p)
-        assert w.shape == (p + 1,) and (w >= 0).all()
-        assert abs(math.fsum(w) - 1.0) <= 1e-12
+    L, hq, hkv, d = 50, 4, 2, 32
+    k = rng.standard_normal((L, hkv, d)) * 4
+    v = rng.standard_normal((L, hkv, d))
+    q = rng.standard_normal((7, hq, d)) * 4
+    pos = np.array([0, 1, 17, 49, 30, 2, 48])
+    out = attend_rows(q, pos, k, v)
+    for h in range(hq):
+        g = kv_head_of(h, hq, hkv)
+        w = weights(q[:, h], pos, k[:, g])
+        assert (w >= 0).all()
+        for i in range(len(pos)):
+            assert abs(math.fsum(w[i]) - 1.0) <= 1e-12
+        np.testing.assert_allclose(w @ v[: w.shape[1], g], out[:, h], rtol=0, atol=1e-13)
 
 
 def test_gqa_equals_mha_with_repeated_kv():

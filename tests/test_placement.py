@@ -69,6 +69,25 @@ def test_oracle_binding_hand_cases():
     assert op.bind([0, 50], [4, 3], 5) == -1
 
 
+def test_oracle_curve_eval_hand_values():
+    """t(L) = c0 + c1 L + c2 L^2, each term checked by hand."""
+    assert op.curve_eval((1.0, 2.0, 3.0), 10) == 321.0           # 1 + 20 + 300
+    assert op.curve_eval((0.5, 0.0, 0.0), 12345) == 0.5
+    assert op.curve_eval((0.0, 0.25, 0.0), 8) == 2.0
+    assert op.curve_eval((0.0, 0.0, 0.125), 4) == 2.0
+    assert op.curve_eval((3.0, -1.0, 0.5), 0) == 3.0
+    assert op.curve_eval((3.0, -1.0, 0.5), 6) == 15.0             # 3 - 6 + 18
+
+
+def test_oracle_admission_quadratic_timeline():
+    # t(L) = 0.5 + 0.25 L + 0.125 L^2 s: L = 2 -> 1.5 s, L = 4 -> 3.5 s
+    a = op.Admission((0.5, 0.25, 0.125), max_wait_s=2.0)
+    assert a.admit(2, 0.0) == (0.0, 1.5)
+    assert a.admit(4, 1.0) == (1.5, 5.0)                           # waits 0.5 s
+    assert a.admit(2, 2.0) is None                                 # would wait 3 s
+    assert a.admit(2, 3.0) == (5.0, 6.5)                           # waits exactly 2 s
+
+
 def test_oracle_admission_hand_timeline():
     a = op.Admission((1.0, 0.0, 0.0), max_wait_s=1.5)     # every prefill takes 1 s
     assert a.admit(100, 0.0) == (0.0, 1.0)

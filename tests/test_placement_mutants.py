@@ -27,6 +27,10 @@ MUTANTS = {
     "curve_no_quadratic_term": ("A = np.stack([np.ones_like(x), x, x * x], axis=1)",
                                 "A = np.stack([np.ones_like(x), x, 0 * x], axis=1)"),
     "curve_wrong_unscaling": ("a[2] / (s * s)", "a[2] / s"),
+    "curve_eval_no_constant": ("return c0 + L * (c1 + L * c2)", "return L * (c1 + L * c2)"),
+    "curve_eval_no_linear": ("return c0 + L * (c1 + L * c2)", "return c0 + L * (L * c2)"),
+    "curve_eval_linear_quadratic": ("return c0 + L * (c1 + L * c2)", "return c0 + L * (c1 + c2)"),
+    "curve_eval_swapped_terms": ("return c0 + L * (c1 + L * c2)", "return c0 + L * (c2 + L * c1)"),
 }
 
 
@@ -68,6 +72,13 @@ def _pins_pass(m):
         bind = m["bind"]
         if (bind([30, 10, 20], [70, 90, 80], 5), bind([20, 30], [80, 270], 5), bind([10, 10, 10], [90, 90, 90], 1),
                 bind([0, 50], [4, 50], 5), bind([0, 50], [4, 3], 5)) != (1, 1, 0, 1, -1):
+            return False
+        ev = m["curve_eval"]
+        if (ev((1.0, 2.0, 3.0), 10), ev((3.0, -1.0, 0.5), 6), ev((0.5, 0.0, 0.0), 7)) != (321.0, 15.0, 0.5):
+            return False
+        q = m["Admission"]((0.5, 0.25, 0.125), 2.0)
+        if (q.admit(2, 0.0), q.admit(4, 1.0), q.admit(2, 2.0), q.admit(2, 3.0)) != (
+                (0.0, 1.5), (1.5, 5.0), None, (5.0, 6.5)):
             return False
         a = m["Admission"]((1.0, 0.0, 0.0), 1.5)
         if (a.admit(100, 0.0), a.admit(100, 0.2), a.admit(100, 0.4)) != ((0.0, 1.0), (1.0, 2.0), None):
