@@ -86,7 +86,8 @@ size_t cs_pool_workspace_bytes(const cs_pool_desc* desc);
 /*
  * Create a pool over caller memory. Physical pages are handed out from a free list shuffled by
  * `placement_seed`, so page placement is random (results never depend on it). Pinned host staging
- * memory for metadata uploads is allocated here and freed by cs_pool_destroy.
+ * memory for metadata uploads is allocated by the pool's first device call (an append, unpack or
+ * attention call) and freed by cs_pool_destroy.
  * Errors: CS_EINVAL (bad descriptor, null/short/misaligned buffers), CS_EHIP.
  */
 cs_status cs_pool_create(const cs_pool_desc* desc, void* kv_base, size_t kv_bytes, void* ws_base,
@@ -165,6 +166,26 @@ cs_status cs_attn_extend(cs_pool* pool, int32_t n_convs, const cs_conv* convs,
  */
 cs_status cs_attn_decode_batch(cs_pool* pool, int32_t n_convs, const cs_conv* convs,
                                int32_t layer, const void* q, void* out, cs_stream stream);
+
+/*
+ * Allocation-free variant of cs_attn_decode_batch, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc). Same
+ * arguments, semantics and output bits as cs_attn_decode_batch; the only difference is where the
+ * decode split keeps its partial records: in a static device array of the library (16 MiB =
+ * 4,194,304 floats on each GPU, held until the process ends) instead of the pool's workspace.
+ * The call allocates no device or pinned memory and creates no HIP objects (the device address of
+ * the array is looked up once per device); host-side planning uses the C++ heap. It launches
+ * untimed: cs_profile_* does not see it.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one GPU (on different
+ * streams, or from different pools on different host threads) race and must not be issued.
+ * Errors: as cs_attn_decode_batch; CS_ENOMEM when the batch's partial records
+ * (n_items * n_q_heads * (head_dim + 4) floats; batches whose conversations are each one work item
+ * need none) exceed the array; CS_ESTATE when the pool has made no device call yet (its first one
+ * allocates its metadata ring; an append or unpack that filled it always has); CS_EINVAL when the
+ * current device is not the pool's.
+ */
+cs_status cs_attn_decode_batch_noalloc(cs_pool* pool, int32_t n_convs, const cs_conv* convs,
+                                       int32_t layer, const void* q, void* out, cs_stream stream);
 
 /*
  * One step of a decoder serving agentic conversations (Section 4: after the one-time transfer a

@@ -26,7 +26,7 @@ EXPORTS = [
     "cs_pool_kv_bytes", "cs_pool_workspace_bytes", "cs_pool_create", "cs_pool_destroy",
     "cs_pool_occupancy", "cs_conv_create", "cs_conv_destroy", "cs_conv_len", "cs_conv_pages",
     "cs_kv_append", "cs_kv_append_batch", "cs_attn_prefill_turn1", "cs_attn_extend",
-    "cs_attn_decode_batch", "cs_mixed_step", "cs_kv_pack_size", "cs_kv_pack", "cs_kv_unpack",
+    "cs_attn_decode_batch", "cs_attn_decode_batch_noalloc", "cs_mixed_step", "cs_kv_pack_size", "cs_kv_pack", "cs_kv_unpack",
     "cs_profile_start",
     "cs_profile_stop", "cs_last_error",
     # placement layer (include/conserve_sched.h)
@@ -84,6 +84,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "cs_attn_prefill_turn1": (I32, [P, I32, PI32, PI32, I32, VP, VP, VP]),
         "cs_attn_extend": (I32, [P, I32, PI32, PI32, I32, VP, VP, VP]),
         "cs_attn_decode_batch": (I32, [P, I32, PI32, I32, VP, VP, VP]),
+        "cs_attn_decode_batch_noalloc": (I32, [P, I32, PI32, I32, VP, VP, VP]),
         "cs_mixed_step": (I32, [P, I32, PI32, PI32, I32, PI32, VP, VP, VP, VP, VP, VP, ctypes.c_uint32, VP]),
         "cs_kv_pack_size": (I32, [P, I32, ctypes.POINTER(SZ)]),
         "cs_kv_pack": (I32, [P, I32, VP, SZ, VP]),
@@ -273,14 +274,20 @@ class KVPool:
         return self._attend(self.lib.cs_attn_extend, convs, q_lens, layer, q, out)
 
     def attn_decode_batch(self, convs, layer, q, out=None) -> torch.Tensor:
+        return self._decode(self.lib.cs_attn_decode_batch, convs, layer, q, out)
+
+    def attn_decode_batch_noalloc(self, convs, layer, q, out) -> torch.Tensor:
+        """cs_attn_decode_batch_noalloc: the caller passes `out` (nothing is allocated)."""
+        return self._decode(self.lib.cs_attn_decode_batch_noalloc, convs, layer, q, out)
+
+    def _decode(self, fn, convs, layer, q, out):
         ca, cp = _i32_array(convs)
         shp = (ca.size, self.n_q_heads, self.head_dim)
         qptr = self._dev(q, "q", shp)
         if out is None:
             out = torch.empty(shp, dtype=torch.bfloat16, device=self.device)
         optr = self._dev(out, "out", shp)
-        _check(self.lib.cs_attn_decode_batch(self._handle, ca.size, cp, layer, qptr, optr,
-                                             _stream_handle(self.device)))
+        _check(fn(self._handle, ca.size, cp, layer, qptr, optr, _stream_handle(self.device)))
         return out
 
     def mixed_step(self, ext_convs, ext_lens, dec_convs, k, v, q_ext=None, q_dec=None,

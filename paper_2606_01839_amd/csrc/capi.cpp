@@ -677,6 +677,52 @@ cs_status cs_attn_decode_batch(cs_pool* p, int32_t n, const cs_conv* convs, int3
   return launch_decode_layer(p, w, layer, q, out);
 }
 
+cs_status cs_attn_decode_batch_noalloc(cs_pool* p, int32_t n, const cs_conv* convs, int32_t layer,
+                                       const void* q, void* out, cs_stream stream) {
+  if (!p) return fail(CS_EINVAL, "null pool");
+  std::vector<const cs::Conv*> cv;
+  cs_status st = check_convs(p, n, convs, cv);
+  if (st != CS_OK) return st;
+  if (layer < 0 || layer >= p->desc.n_layers) return fail(CS_ERANGE, "layer out of range");
+  for (int32_t i = 0; i < n; ++i)
+    if (cv[i]->len < 1) return fail(CS_ESTATE, "decode on an empty conversation");
+  if (n == 0) return CS_OK;
+  if (!q || !out) return fail(CS_EINVAL, "null q/out");
+  // The pool's device state (metadata ring) is created by its first device call, which allocates;
+  // every pool holding a non-empty conversation has made one (an append or an unpack).
+  if (!p->dev_ready) return fail(CS_ESTATE, "pool has no device state yet (no append or unpack ran)");
+  int dev = -1;
+  CS_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev != p->device) return fail(CS_EINVAL, "the current device is not the pool's device");
+  std::vector<int32_t> slots(n);
+  std::vector<int64_t> lens(n);
+  for (int32_t i = 0; i < n; ++i) {
+    slots[i] = cs::ConvTable::slot_of(convs[i]);
+    lens[i] = cv[i]->len;
+  }
+  const cs::DecodePlan plan = plan_decode_batch(p, slots, lens);
+  const size_t need = plan.single_item ? 0
+      : static_cast<size_t>(plan.n_items) * p->desc.n_q_heads * cs::partial_floats(p->desc.head_dim);
+  if (need > cs::kStaticScratchFloats)
+    return fail(CS_ENOMEM, "decode partials (" + std::to_string(need * 4) + " bytes) exceed the " +
+                               std::to_string(cs::kStaticScratchFloats * 4) + "-byte static scratch");
+  if (decode_upload_bytes(plan) > kQuarter) return fail(CS_ENOMEM, "batch descriptor exceeds the metadata ring");
+  float* scratch = nullptr;
+  CS_HIP(cs::static_decode_scratch(&scratch), "hipGetSymbolAddress(decode scratch)");
+  if ((st = use_stream(p, as_stream(stream))) != CS_OK) return st;
+  DecodeWork w;
+  if ((st = upload2(p, plan.convs, plan.order, &w.convs, &w.order)) != CS_OK) return st;
+  const cs::PoolGeom g = p->geom();
+  // untimed launches: the timing events of cs_profile_* would be created on demand
+  CS_HIP(cs::launch_decode_split(g, layer, w.convs, w.order, static_cast<int>(plan.convs.size()), plan.n_items,
+                                 plan.split_tokens, q, scratch, plan.single_item ? out : nullptr, p->stream),
+         "decode split launch");
+  if (plan.single_item) return CS_OK;
+  CS_HIP(cs::launch_decode_merge(g, w.convs, static_cast<int>(plan.convs.size()), scratch, out, p->stream),
+         "decode merge launch");
+  return CS_OK;
+}
+
 cs_status cs_kv_pack_size(const cs_pool* p, cs_conv conv, size_t* bytes) {
   if (!p || !bytes) return fail(CS_EINVAL, "null argument");
   const cs::Conv* c = p->convs.find(conv);

@@ -17,10 +17,39 @@
 // order and there are no atomics: bitwise deterministic, and split boundaries are logical
 // positions, so results do not depend on physical page placement.
 #include <cmath>
+#include <mutex>
 
 #include "decode_split.hpp"
 
 namespace cs {
+
+namespace {
+// Static decode scratch of the allocation-free decode entry point: the split partial records live
+// here instead of in the pool's workspace. Each GPU the library runs on holds its own copy until
+// the process ends. Host code never passes `scratch` itself to a kernel (on the host it is only a
+// stand-in symbol): its device address, per device, comes from hipGetSymbolAddress below.
+__device__ __align__(256) float scratch[kStaticScratchFloats];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_dev[kMaxDevices] = {};
+}  // namespace
+
+hipError_t static_decode_scratch(float** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));   // with `dev` current: this device's copy
+    if (e != hipSuccess) return e;
+    g_scratch_dev[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
 
 // Log-sum-exp merge of the item records of one (conversation b, query head h) by 256 threads (`tid`
 // in 0 .. 255, LDS `lds`), in three steps whose order depends only on the record count (bitwise

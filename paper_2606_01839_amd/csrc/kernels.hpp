@@ -50,6 +50,12 @@ hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const D
                                      float* split_partials, const float* merge_partials,
                                      void* merge_out, hipStream_t stream);
 
+// Capacity of the static decode scratch (floats): 16 MiB on each GPU.
+constexpr size_t kStaticScratchFloats = size_t(4) << 20;
+// Device address of the static decode scratch on the current device (looked up once per device
+// with hipGetSymbolAddress and cached; allocates nothing).
+hipError_t static_decode_scratch(float** out);
+
 // One layer of a mixed step in one launch (head_dim 128 only): the extend tiles of the layer and
 // its decode split (partials; the merge follows as launch_decode_merge).
 hipError_t launch_mixed_layer(const PoolGeom& g, int layer, const ExtendConvDesc* d_ext_convs,
