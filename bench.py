@@ -37,9 +37,16 @@ from synth.traces import (DecodeBatch, ExtendBatch, MixedTrace, PrefillTransfer,
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
 METRIC = "decode-attn HBM GB/s + extend/prefill TFLOP/s, each as % of MI355X peak"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_split_traffic.json")
-KERNEL_SOURCES = ["paper_2606_01839_amd/csrc/decode.hip", "paper_2606_01839_amd/csrc/decode_split.hpp",
-                  "paper_2606_01839_amd/csrc/device_common.hpp"]
+PROFILES = os.path.join(ROOT, "profiles")
+# The sources each kernel is built from: counters committed under profiles/ apply only while these
+# are unchanged (their SHA-256 is stored with the counters).
+KERNEL_SOURCES = {
+    "decode_split": ["paper_2606_01839_amd/csrc/decode.hip", "paper_2606_01839_amd/csrc/decode_split.hpp",
+                     "paper_2606_01839_amd/csrc/device_common.hpp"],
+    "attn_fwd": ["paper_2606_01839_amd/csrc/attn_fwd.hip", "paper_2606_01839_amd/csrc/decode_split.hpp",
+                 "paper_2606_01839_amd/csrc/device_common.hpp"],
+    "kv_move": ["paper_2606_01839_amd/csrc/kv_move.hip", "paper_2606_01839_amd/csrc/device_common.hpp"],
+}
 
 
 def log(*a):
@@ -60,25 +67,35 @@ def gen_q(seed, conv, start, n, hq, d, device="cuda"):
                           device=device)
 
 
-def source_hash() -> str:
+def source_hash(group: str) -> str:
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[group]:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
-def traffic_per_launch(workload: str):
-    """HBM bytes per decode-split launch from committed rocprofv3 counters, if the kernel source
-    is unchanged since they were taken (else None)."""
+def kernel_counters(name: str, workload: str, group: str, alg_bytes=None) -> dict:
+    """Figures from the committed rocprofv3 counters of a kernel (profiles/<name>_counters.json):
+    HBM traffic per launch (FETCH_SIZE and WRITE_SIZE, each calibrated on a 1 GiB device copy in
+    the same run) and, for the attention kernel, its matrix-core busy fraction, sustained clock and
+    LDS bank-conflict cycles. Only when the file was taken on this workload and on the kernel's
+    current sources; otherwise traffic is None."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(os.path.join(PROFILES, f"{name}_counters.json")) as f:
             t = json.load(f)
     except (OSError, ValueError):
-        return None
-    if t.get("source_sha256") != source_hash() or t.get("workload") != workload:
-        return None
-    return t.get("traffic_bytes_per_launch")
+        return {"traffic": None}
+    if t.get("source_sha256") != source_hash(group) or t.get("workload") != workload:
+        return {"traffic": None, "counters_note": f"profiles/{name}_counters.json was taken on other "
+                                                  "sources or another workload"}
+    out = {"traffic": t.get("traffic_bytes_per_launch"), "counters_file": f"profiles/{name}_counters.json"}
+    if alg_bytes and out["traffic"]:
+        out["traffic_over_algorithmic"] = out["traffic"] / alg_bytes
+    for k in ("mfma_busy", "sustained_clock_ghz", "lds_bank_conflict_cycles_per_launch"):
+        if k in t:
+            out[k] = t[k]
+    return out
 
 
 def energy_run(fn, seconds=8.0):
@@ -141,6 +158,61 @@ def blas_threads() -> int:
     return len(os.sched_getaffinity(0))
 
 
+def host_info() -> dict:
+    """CPU model, usable cores and the BLAS library numpy calls (the CPU baseline's machine)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                blas = {"library": i.get("internal_api"), "version": i.get("version"),
+                        "threads": i.get("num_threads"), "architecture": i.get("architecture")}
+                break
+    except Exception:
+        pass
+    return {"cpu_model": model, "usable_cores": len(os.sched_getaffinity(0)), "blas": blas}
+
+
+def device_block() -> dict:
+    """hipDeviceProp figures of the GPU and a streaming-read probe: 4 GiB read once with the
+    non-temporal 16-byte loads of the decode and pack kernels, 8 workgroups per CU (median of 10
+    after 3 warm-ups, HIP events on the probe's stream)."""
+    from paper_2606_01839_amd import device_info, probe_stream_read
+    info = device_info(0)
+    buf = torch.empty(4 << 30, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    sink = torch.zeros(4, dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        probe_stream_read(buf, sink)
+    ts = []
+    for _ in range(10):
+        a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a_.record()
+        probe_stream_read(buf, sink)
+        b_.record()
+        torch.cuda.synchronize()
+        ts.append(a_.elapsed_time(b_))
+    ms = float(np.median(ts))
+    del buf, sink
+    torch.cuda.empty_cache()
+    return {"name": info["name"], "arch": info["arch"], "cu_count": info["cu_count"],
+            "clock_mhz": info["clock_khz"] / 1e3, "memory_clock_mhz": info["memory_clock_khz"] / 1e3,
+            "memory_bus_width_bits": info["memory_bus_width_bits"],
+            "lds_per_cu_kib": info["lds_per_cu_bytes"] / 1024, "l2_mib": info["l2_bytes"] / 2**20,
+            "hbm_gib": info["total_mem_bytes"] / 2**30,
+            "stream_read_probe": {"bytes": 4 << 30, "ms": ms, "gbs": (4 << 30) / (ms * 1e-3) / 1e9,
+                                  "frac_of_peak": (4 << 30) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}}
+
+
 def sample_rows(n: int, seed: int, k: int = 4):
     """Query rows 0 .. n-1 to check and time: first and last, rows around the 16-token page and
     64-row tile boundaries nearest the middle, and k seeded random rows (sorted, distinct)."""
@@ -165,7 +237,7 @@ def oracle_rows(kv, q_rows, out_rows, pos, hq, d):
 def oracle_baseline(flops, secs, total_flops, sample):
     rate = flops / secs
     return {"value": rate / 1e12, "unit": "TFLOP/s", "cores": blas_threads(), "kind": "oracle",
-            "sample": sample, "full_batch_s_extrapolated": total_flops / rate}
+            "sample": sample, "full_batch_s_extrapolated": total_flops / rate, **host_info()}
 
 
 # ------------------------------------------------------------------------------------------------
@@ -312,7 +384,7 @@ def bench_decode(args):
     workload = (f"decode batch: {len(lens)} conversations, context U[{tr.lo},{tr.hi}] (sum "
                 f"{int(lens.sum())} tokens), {hq}q/{hkv}kv heads, head_dim {d}, bf16 K/V x per-head "
                 f"scale U[{tr.scale_lo},{tr.scale_hi}], 16-token pages randomly placed, 1 layer")
-    traffic = traffic_per_launch(workload)
+    counters = kernel_counters("decode_split", workload, "decode_split", split_bytes)
     res = {
         "ms_per_step": ms,
         "step_ms_p10_p50_p90": [float(np.percentile(step_ms, x)) for x in (10, 50, 90)],
@@ -322,14 +394,14 @@ def bench_decode(args):
         "split_bytes": split_bytes,
         "step_bytes": step_bytes,
         "workload": workload,
-        "traffic": traffic,
+        "counters": counters,
         "energy": None if not en or not en["avg_watts"] else {
             **en, "tokens_per_joule": en["calls"] * len(lens) / en["wall_s"] / en["avg_watts"],
             "gb_per_joule": en["calls"] * step_bytes / 1e9 / en["wall_s"] / en["avg_watts"]},
         "parity": {"convs": len(lens), "max_abs": max_abs, "rel_l2": rel_l2,
                    "ok": bool(max_abs <= 1e-2 and rel_l2 <= 3e-3)},
         "cpu": {"value": passes * step_bytes / cpu_s / 1e9, "unit": "GB/s", "cores": blas_threads(),
-                "kind": "oracle",
+                "kind": "oracle", **host_info(),
                 "sample": f"fp64 oracle over all {len(lens)} conversations x {hq} heads of the same "
                           f"decode step (inputs already in host memory as fp64), {passes} passes "
                           f"in {cpu_s:.1f} s"},
@@ -384,23 +456,96 @@ def bench_extend(args):
     pool.close()
     del kcat, vcat
     torch.cuda.empty_cache()
+    workload = (f"extend-prefill: {tr.n_convs} conversations, prefix U[{tr.prefix_lo},{tr.prefix_hi}], chunk "
+                f"logN(median {tr.chunk_median}) in [{tr.chunk_lo},{tr.chunk_hi}] (sum {int(chunk.sum())}), "
+                f"{hq}q/{hkv}kv, d {d}")
+    app_workload = f"kv_append of the {int(chunk.sum())} new tokens of the extend batch (1 layer)"
     return {
-        "extend": {"workload": f"extend-prefill: {tr.n_convs} conversations, prefix U[{tr.prefix_lo},"
-                               f"{tr.prefix_hi}], chunk logN(median {tr.chunk_median}) in "
-                               f"[{tr.chunk_lo},{tr.chunk_hi}] (sum {int(chunk.sum())}), {hq}q/{hkv}kv, d {d}",
+        "extend": {"workload": workload,
                    "ms": ms, "kernel_ms": fwd_ms, "flops": flops,
                    "tflops": flops / (ms * 1e-3) / 1e12,
                    "roofline": {"bound": "mfma", "achieved": flops / (fwd_ms * 1e-3) / 1e12,
                                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                                "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
+                                "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+                                **kernel_counters("attn_fwd_extend", workload, "attn_fwd")},
                    "spot_parity_ok": bool(ok), "spot_max_abs": err, "cpu_oracle": cpu},
-        "append": {"workload": f"kv_append of the {int(chunk.sum())} new tokens of the extend batch",
+        "append": {"workload": app_workload,
                    "kernel_ms": app[0], "bytes": app_bytes,
                    "gbs": app_bytes / (app[0] * 1e-3) / 1e9,
                    "roofline": {"bound": "hbm", "achieved": app_bytes / (app[0] * 1e-3) / 1e9,
                                 "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                                "frac": app_bytes / (app[0] * 1e-3) / 1e9 / HBM_PEAK_GBS}},
+                                "frac": app_bytes / (app[0] * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                **kernel_counters("kv_append_extend", app_workload, "kv_move", app_bytes)}},
     }
+
+
+def bench_append(args):
+    """kv_append in a decoder pool of the mixed trace's shape (32 layers, 32q/8kv, d 128): 64
+    conversations with cached contexts U[1000, 3000] (so most last pages are partly filled) receive
+    (a) one decoded token each for every layer -- the append of a decode step, 20 steps in a row --
+    and (b) one extend chunk each, 16 of them with logN(median 1024) lengths in [128, 4096].
+    Algorithmic bytes: the new K and V read once and written once (2 x 4096 B per token and layer)."""
+    from paper_2606_01839_amd import KVPool
+    NL, hq, hkv, d, seed, B, steps = 32, 32, 8, 128, 1008, 64, 20
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(1000, 3001, size=B)
+    chunks = np.clip(np.exp(rng.normal(math.log(1024), 0.7, size=16)).astype(np.int64), 128, 4096)
+    tok_bytes = NL * 2 * hkv * d * 2                     # K + V of one token, all layers
+    pool = KVPool(NL, hq, hkv, d, n_pages=int(sum(pages_for(int(L) + steps + 4096) for L in lens)) + 64,
+                  max_convs=B, max_pages_per_conv=pages_for(3000 + steps + 4096), placement_seed=seed)
+    convs = [pool.conv_create() for _ in range(B)]
+    for b0 in range(0, B, 16):                           # untimed fill (zeros: the bytes do not matter)
+        n = [int(L) for L in lens[b0:b0 + 16]]
+        z = torch.zeros((NL, sum(n), hkv, d), dtype=torch.bfloat16, device="cuda")
+        pool.kv_append_batch(convs[b0:b0 + 16], n, z, z)
+        del z
+    kd = [sv.bf16_tensor(sv.mix_key(seed, s_, KIND_K, 0), (NL, B, hkv, d), device="cuda") for s_ in range(steps)]
+    vd = [sv.bf16_tensor(sv.mix_key(seed, s_, KIND_V, 0), (NL, B, hkv, d), device="cuda") for s_ in range(steps)]
+    torch.cuda.synchronize()
+    pool.profile_start()
+    for s_ in range(steps):
+        pool.kv_append_batch(convs, [1] * B, kd[s_], vd[s_])
+    dec = pool.profile_stop()["append"]
+    sel = convs[:16]
+    kc = sv.bf16_tensor(sv.mix_key(seed, 99, KIND_K, 0), (NL, int(chunks.sum()), hkv, d), device="cuda")
+    vc = sv.bf16_tensor(sv.mix_key(seed, 99, KIND_V, 0), (NL, int(chunks.sum()), hkv, d), device="cuda")
+    torch.cuda.synchronize()
+    pool.profile_start()
+    pool.kv_append_batch(sel, [int(c) for c in chunks], kc, vc)
+    ext = pool.profile_stop()["append"]
+    # bit-exactness of the last decode step's token and of the chunks, read back through the pool
+    ok = True
+    view = pool.kv_view()
+    for b in (0, B - 1):
+        pages = pool.conv_pages(convs[b])
+        L = int(lens[b]) + steps - 1                      # position of the last decoded token
+        blk = view[:, int(pages[L // 16])].cpu()          # [NL][Hkv][16 * 2 * d]
+        t = L % 16
+        k_got = blk[:, :, :16 * d].view(NL, hkv, d // 32, 16, 32)[:, :, :, t, :].reshape(NL, hkv, d)
+        v_got = blk[:, :, 16 * d:].view(NL, hkv, d, 16)[:, :, :, t]
+        ok = ok and torch.equal(k_got, kd[-1][:, b].cpu().view(torch.int16)) and \
+            torch.equal(v_got, vd[-1][:, b].cpu().view(torch.int16))
+    pool.close()
+    del kd, vd, kc, vc
+    torch.cuda.empty_cache()
+    dec_bytes = 2 * B * tok_bytes
+    ext_bytes = 2 * int(chunks.sum()) * tok_bytes
+    gbs = lambda b, ms: b / (ms * 1e-3) / 1e9
+    wl_dec = f"kv_append of one decoded token for each of {B} conversations (context U[1000,3000]), {NL} layers, {hkv} kv heads, d {d}"
+    wl_ext = (f"kv_append of 16 extend chunks logN(median 1024) in [128,4096] (sum {int(chunks.sum())}) into "
+              f"conversations of context U[1000,3000], {NL} layers, {hkv} kv heads, d {d}")
+    return {"append_decode_step": {
+                "workload": wl_dec, "launches": dec[1], "kernel_ms_per_step": dec[0] / dec[1],
+                "bytes_per_step": dec_bytes, "gbs": gbs(dec_bytes, dec[0] / dec[1]),
+                "last_token_bit_exact": bool(ok),
+                "roofline": {"bound": "hbm", "achieved": gbs(dec_bytes, dec[0] / dec[1]), "peak": HBM_PEAK_GBS,
+                             "unit": "GB/s", "frac": gbs(dec_bytes, dec[0] / dec[1]) / HBM_PEAK_GBS,
+                             **kernel_counters("kv_append_decode", wl_dec, "kv_move", dec_bytes)}},
+            "append_chunks": {
+                "workload": wl_ext, "kernel_ms": ext[0], "bytes": ext_bytes, "gbs": gbs(ext_bytes, ext[0]),
+                "roofline": {"bound": "hbm", "achieved": gbs(ext_bytes, ext[0]), "peak": HBM_PEAK_GBS,
+                             "unit": "GB/s", "frac": gbs(ext_bytes, ext[0]) / HBM_PEAK_GBS,
+                             **kernel_counters("kv_append_chunks", wl_ext, "kv_move", ext_bytes)}}}
 
 
 def chunked_prefill(tr, lens, q, out_one_shot, mk, chunk=8192):
@@ -456,7 +601,10 @@ def chunked_prefill(tr, lens, q, out_one_shot, mk, chunk=8192):
             "bitwise_equal_to_one_shot": bool(same)}
 
 
-def bench_prefill_transfer(args):
+def bench_prefill_transfer(args, parts=("prefill", "chunked", "transfer")):
+    """Turn-1 prefill batch: the one-shot prefill ("prefill"), the same batch in 8192-token chunks
+    ("chunked") and the one-time transfer of every conversation ("transfer"); `parts` picks which
+    run (a profiler run of one part then sees only that part's kernels)."""
     from paper_2606_01839_amd import KVPool
     tr = PrefillTransfer()
     sh = tr.shape
@@ -465,6 +613,20 @@ def bench_prefill_transfer(args):
     npg = pre.desc.n_pages
     mk = lambda seed: KVPool(1, hq, hkv, d, n_pages=npg, max_convs=tr.n_convs,
                              max_pages_per_conv=pages_for(tr.hi), placement_seed=seed)
+    res = {}
+    if "prefill" in parts or "chunked" in parts:
+        res.update(_prefill_parts(args, tr, pre, convs, lens, q, mk, parts))
+    if "transfer" in parts:
+        res.update(_transfer_part(tr, pre, convs, lens, mk))
+    pre.close()
+    del q
+    torch.cuda.empty_cache()
+    return res
+
+
+def _prefill_parts(args, tr, pre, convs, lens, q, mk, parts):
+    sh = tr.shape
+    hq, hkv, d = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
     out = torch.empty_like(q)
     step = lambda: pre.attn_prefill_turn1(convs, lens, 0, q, out)
     reps = 2
@@ -488,8 +650,31 @@ def bench_prefill_transfer(args):
     cpu = oracle_baseline(s_flops, secs, flops, f"fp64 oracle on {n_rows} sampled query rows (all {hq} "
                           f"heads) of conversations {picks[0]} and {picks[1]} (the two shortest), "
                           f"{secs:.1f} s; the full batch time is extrapolated at that rate")
-    chunked = chunked_prefill(tr, lens, q, out, mk)
-    # one-time transfer: pack every conversation, unpack into a pool with other placement
+    workload = f"turn-1 prefill: {tr.n_convs} conversations, L U[{tr.lo},{tr.hi}] (sum {int(lens.sum())}), {hq}q/{hkv}kv, d {d}"
+    res = {
+        "prefill": {"workload": workload,
+                    "ms": ms, "kernel_ms": fwd_ms, "flops": flops,
+                    "tflops": flops / (ms * 1e-3) / 1e12,
+                    "roofline": {"bound": "mfma", "achieved": flops / (fwd_ms * 1e-3) / 1e12,
+                                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                 "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+                                 **kernel_counters("attn_fwd_prefill", workload, "attn_fwd")},
+                    "spot_parity_ok": bool(err <= 1e-2), "spot_max_abs": err, "cpu_oracle": cpu},
+        "prefill_energy": None if not en or not en["avg_watts"] else {
+            **en, "tokens_per_joule": en["calls"] * int(lens.sum()) / en["wall_s"] / en["avg_watts"],
+            "tflop_per_joule": en["calls"] * flops / 1e12 / en["wall_s"] / en["avg_watts"]},
+    }
+    if "chunked" in parts:
+        res["prefill_chunked"] = chunked_prefill(tr, lens, q, out, mk)
+    del out
+    return res
+
+
+def _transfer_part(tr, pre, convs, lens, mk):
+    """Pack every conversation of the prefill batch, unpack into a pool with another placement,
+    and check pack -> unpack -> pack is bit-exact."""
+    sh = tr.shape
+    hkv, d = sh.n_kv_heads, sh.head_dim
     dst = mk(tr.dst_seed)
     wires = [torch.empty(pre.kv_pack_size(c), dtype=torch.uint8, device="cuda") for c in convs]
     pre.profile_start()
@@ -504,30 +689,23 @@ def bench_prefill_transfer(args):
         ok = ok and torch.equal(dst.kv_pack(c), w)
     torch.cuda.synchronize()
     move = 2 * int(lens.sum()) * 2 * hkv * d * 2          # read + write of every valid token's K, V
-    pre.close()
     dst.close()
-    del wires, q, out
+    del wires
     torch.cuda.empty_cache()
     gbs = lambda b, t: b / (t * 1e-3) / 1e9
+    workload = (f"one-time transfer of the turn-1 prefill batch: {tr.n_convs} conversations, L U[{tr.lo},"
+                f"{tr.hi}] (sum {int(lens.sum())}), {hkv} kv heads, d {d}, 1 layer")
     return {
-        "prefill": {"workload": f"turn-1 prefill: {tr.n_convs} conversations, L U[{tr.lo},{tr.hi}] "
-                                f"(sum {int(lens.sum())}), {hq}q/{hkv}kv, d {d}",
-                    "ms": ms, "kernel_ms": fwd_ms, "flops": flops,
-                    "tflops": flops / (ms * 1e-3) / 1e12,
-                    "roofline": {"bound": "mfma", "achieved": flops / (fwd_ms * 1e-3) / 1e12,
-                                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                                 "frac": flops / (fwd_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
-                    "spot_parity_ok": bool(err <= 1e-2), "spot_max_abs": err, "cpu_oracle": cpu},
-        "prefill_energy": None if not en or not en["avg_watts"] else {
-            **en, "tokens_per_joule": en["calls"] * int(lens.sum()) / en["wall_s"] / en["avg_watts"],
-            "tflop_per_joule": en["calls"] * flops / 1e12 / en["wall_s"] / en["avg_watts"]},
-        "prefill_chunked": chunked,
-        "pack": {"kernel_ms": pk[0], "launches": pk[1], "bytes": move, "gbs": gbs(move, pk[0]),
+        "pack": {"workload": workload, "kernel_ms": pk[0], "launches": pk[1], "bytes": move,
+                 "gbs": gbs(move, pk[0]),
                  "roofline": {"bound": "hbm", "achieved": gbs(move, pk[0]), "peak": HBM_PEAK_GBS,
-                              "unit": "GB/s", "frac": gbs(move, pk[0]) / HBM_PEAK_GBS}},
-        "unpack": {"kernel_ms": up[0], "launches": up[1], "bytes": move, "gbs": gbs(move, up[0]),
+                              "unit": "GB/s", "frac": gbs(move, pk[0]) / HBM_PEAK_GBS,
+                              **kernel_counters("kv_pack", workload, "kv_move", move / pk[1])}},
+        "unpack": {"workload": workload, "kernel_ms": up[0], "launches": up[1], "bytes": move,
+                   "gbs": gbs(move, up[0]),
                    "roofline": {"bound": "hbm", "achieved": gbs(move, up[0]), "peak": HBM_PEAK_GBS,
-                                "unit": "GB/s", "frac": gbs(move, up[0]) / HBM_PEAK_GBS},
+                                "unit": "GB/s", "frac": gbs(move, up[0]) / HBM_PEAK_GBS,
+                                **kernel_counters("kv_unpack", workload, "kv_move", move / up[1])},
                    "round_trip_bit_exact": bool(ok)},
     }
 
@@ -958,8 +1136,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--skip-components", action="store_true")
-    ap.add_argument("--only", choices=["decode", "extend", "prefill", "mixed", "curve", "shapes", "overlap",
-                                           "dcurve"], default=None,
+    ap.add_argument("--only", choices=["decode", "extend", "prefill", "prefill1", "transfer", "append", "mixed",
+                                       "curve", "shapes", "overlap", "dcurve", "device"], default=None,
                     help="run one component and print only its JSON (for profiling)")
     ap.add_argument("--mixed-steps", type=int, default=400,
                     help="timed steps of the mixed agentic trace component (0 = skip it)")
@@ -980,15 +1158,20 @@ def main():
         copy_calibration()
     if args.only and args.only != "decode":
         fn = {"extend": bench_extend, "prefill": bench_prefill_transfer, "mixed": bench_mixed,
+              "prefill1": lambda a: bench_prefill_transfer(a, parts=("prefill",)),
+              "transfer": lambda a: bench_prefill_transfer(a, parts=("transfer",)),
+              "append": bench_append, "device": lambda a: {"device": device_block(), "host": host_info()},
               "curve": bench_prefill_curve, "shapes": bench_gqa_shapes,
               "overlap": bench_transfer_overlap, "dcurve": bench_decode_curve}[args.only]
         print(json.dumps({"component": args.only, **fn(args)}), flush=True)
         return
+    device = device_block()
     dec = bench_decode(args)
     comps = {}
     if not args.skip_components and not args.only:
         comps.update(bench_extend(args))
         comps.update(bench_prefill_transfer(args))
+        comps.update(bench_append(args))
         comps.update(bench_prefill_curve(args))
         comps.update(bench_gqa_shapes(args))
         comps.update(bench_transfer_overlap(args))
@@ -1013,10 +1196,11 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "kernel": "decode_split_kernel<128>",
                      "achieved": round(split_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(split_gbs / HBM_PEAK_GBS, 4), "traffic": dec["traffic"],
+                     "frac": round(split_gbs / HBM_PEAK_GBS, 4), **dec["counters"],
                      "algorithmic_bytes_per_launch": dec["split_bytes"],
                      "kernel_ms": round(dec["split_ms"], 4), "merge_kernel_ms": round(dec["merge_ms"], 4)},
         "cpu_baseline": dec["cpu"],
+        "device": device,
         "parity": dec["parity"],
         "step_ms_p10_p50_p90": dec["step_ms_p10_p50_p90"],
         "energy": dec["energy"],

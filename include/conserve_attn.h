@@ -265,6 +265,34 @@ enum {
 cs_status cs_profile_start(cs_pool* pool);
 cs_status cs_profile_stop(cs_pool* pool, double* ms, int64_t* launches);
 
+/*
+ * Instrumentation: properties of a HIP device that measurements are logged with (from
+ * hipGetDeviceProperties). Errors: CS_EINVAL (null), CS_EHIP (no such device).
+ */
+typedef struct {
+  char name[256];
+  char arch[64];                 /* gcnArchName, e.g. "gfx950:sramecc+:xnack-" */
+  int32_t cu_count;              /* compute units */
+  int32_t clock_khz;             /* peak engine clock */
+  int32_t memory_clock_khz;      /* peak memory clock */
+  int32_t memory_bus_width_bits;
+  int64_t lds_per_cu_bytes;      /* shared memory per compute unit */
+  int64_t lds_per_block_bytes;   /* shared memory one workgroup may use */
+  int64_t l2_bytes;              /* L2 cache size the runtime reports */
+  int64_t total_mem_bytes;
+} cs_device_info_t;
+cs_status cs_device_info(int32_t device, cs_device_info_t* out);
+
+/*
+ * Instrumentation: read `bytes` (a multiple of 16) of device memory at `src` once with the
+ * non-temporal 16-byte loads the decode and pack kernels use, on 8 workgroups per compute unit of
+ * the current device, enqueued on `stream`; `sink` is 4 bytes of device memory that the kernel
+ * writes only if the XOR of everything read equals 0x9E3779B9 (it exists so the loads stay live).
+ * Time it with events on `stream` to get what streaming reads reach on the part.
+ * Errors: CS_EINVAL (null pointers, bytes not a multiple of 16), CS_EHIP.
+ */
+cs_status cs_probe_stream_read(const void* src, size_t bytes, void* sink, cs_stream stream);
+
 /* Message of the last failing call on this thread ("" if none). Valid until the next call. */
 const char* cs_last_error(void);
 

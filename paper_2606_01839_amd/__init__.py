@@ -7,4 +7,4 @@ from .conserve import (KVPool, ConserveError, load_library, PAGE_TOKENS, EXPORTS
                        CS_OK, CS_EINVAL, CS_ENOMEM, CS_ENOENT, CS_ESTATE, CS_ERANGE, CS_EHIP, CS_EBUSY,
                        CS_MIXED_LAYER_ORDERED,
                        Scheduler, prefill_curve_fit, prefill_curve_eval, provision_decoders,
-                       place_least_occupied)
+                       place_least_occupied, device_info, probe_stream_read)

@@ -17,7 +17,8 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libconserve_attn.so")
 BUILD = os.path.join(PKG, "_build")
 
-SOURCES = ["host/host_state.cpp", "host/sched.cpp", "capi.cpp", "sched_capi.cpp", "kv_move.hip", "decode.hip", "attn_fwd.hip"]
+SOURCES = ["host/host_state.cpp", "host/sched.cpp", "capi.cpp", "sched_capi.cpp", "kv_move.hip", "decode.hip", "attn_fwd.hip",
+           "probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -28,7 +28,7 @@ EXPORTS = [
     "cs_kv_append", "cs_kv_append_batch", "cs_attn_prefill_turn1", "cs_attn_extend",
     "cs_attn_decode_batch", "cs_attn_decode_batch_noalloc", "cs_mixed_step", "cs_kv_pack_size", "cs_kv_pack", "cs_kv_unpack",
     "cs_profile_start",
-    "cs_profile_stop", "cs_last_error",
+    "cs_profile_stop", "cs_device_info", "cs_probe_stream_read", "cs_last_error",
     # placement layer (include/conserve_sched.h)
     "cs_prefill_curve_fit", "cs_prefill_curve_eval", "cs_provision_decoders",
     "cs_place_least_occupied", "cs_sched_create", "cs_sched_destroy", "cs_sched_admit",
@@ -48,6 +48,14 @@ class PoolDesc(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("max_convs", ctypes.c_int32), ("max_pages_per_conv", ctypes.c_int32),
                 ("n_pages", ctypes.c_int64)]
+
+
+class DeviceInfo(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 256), ("arch", ctypes.c_char * 64),
+                ("cu_count", ctypes.c_int32), ("clock_khz", ctypes.c_int32),
+                ("memory_clock_khz", ctypes.c_int32), ("memory_bus_width_bits", ctypes.c_int32),
+                ("lds_per_cu_bytes", ctypes.c_int64), ("lds_per_block_bytes", ctypes.c_int64),
+                ("l2_bytes", ctypes.c_int64), ("total_mem_bytes", ctypes.c_int64)]
 
 
 class PrefillCurve(ctypes.Structure):
@@ -91,6 +99,8 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "cs_kv_unpack": (I32, [P, VP, SZ, I64, PI32, VP]),
         "cs_profile_start": (I32, [P]),
         "cs_profile_stop": (I32, [P, ctypes.POINTER(ctypes.c_double), PI64]),
+        "cs_device_info": (I32, [I32, ctypes.POINTER(DeviceInfo)]),
+        "cs_probe_stream_read": (I32, [VP, SZ, VP, VP]),
         "cs_last_error": (ctypes.c_char_p, []),
         "cs_prefill_curve_fit": (I32, [I32, PI64, ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(PrefillCurve), ctypes.POINTER(ctypes.c_double)]),
@@ -357,6 +367,30 @@ class KVPool:
         _check(self.lib.cs_kv_unpack(self._handle, src.data_ptr(), src.numel() * src.element_size(),
                                      n_tokens, ctypes.byref(c), _stream_handle(self.device)))
         return c.value
+
+
+# ------------------------------------------------------------------------------------------------
+# instrumentation
+# ------------------------------------------------------------------------------------------------
+def device_info(device: int = 0) -> dict:
+    """cs_device_info: name, arch, CU count, clocks, LDS, L2 and memory size of a HIP device."""
+    lib = load_library()
+    d = DeviceInfo()
+    _check(lib.cs_device_info(int(device), ctypes.byref(d)))
+    out = {f: getattr(d, f) for f, _ in DeviceInfo._fields_}
+    out["name"], out["arch"] = d.name.decode(), d.arch.decode()
+    return out
+
+
+def probe_stream_read(src: torch.Tensor, sink: torch.Tensor) -> None:
+    """cs_probe_stream_read over a contiguous device tensor (its byte size rounded down to 16) on
+    the current stream; sink: >= 4 bytes of device memory."""
+    lib = load_library()
+    if src.device.type != "cuda" or not src.is_contiguous() or sink.device.type != "cuda":
+        raise ValueError("src and sink must be contiguous device tensors")
+    nbytes = (src.numel() * src.element_size()) // 16 * 16
+    _check(lib.cs_probe_stream_read(src.data_ptr(), nbytes, sink.data_ptr(),
+                                    _stream_handle(src.device)))
 
 
 # ------------------------------------------------------------------------------------------------

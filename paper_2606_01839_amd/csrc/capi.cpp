@@ -945,6 +945,35 @@ cs_status cs_mixed_step(cs_pool* p, int32_t n_ext, const cs_conv* ext_convs, con
   return st;
 }
 
+cs_status cs_device_info(int32_t device, cs_device_info_t* out) {
+  if (!out) return fail(CS_EINVAL, "null out");
+  hipDeviceProp_t pr;
+  CS_HIP(hipGetDeviceProperties(&pr, device), "hipGetDeviceProperties");
+  std::memset(out, 0, sizeof(*out));
+  std::strncpy(out->name, pr.name, sizeof(out->name) - 1);
+  std::strncpy(out->arch, pr.gcnArchName, sizeof(out->arch) - 1);
+  out->cu_count = pr.multiProcessorCount;
+  out->clock_khz = pr.clockRate;
+  out->memory_clock_khz = pr.memoryClockRate;
+  out->memory_bus_width_bits = pr.memoryBusWidth;
+  out->lds_per_cu_bytes = static_cast<int64_t>(pr.maxSharedMemoryPerMultiProcessor);
+  out->lds_per_block_bytes = static_cast<int64_t>(pr.sharedMemPerBlock);
+  out->l2_bytes = pr.l2CacheSize;
+  out->total_mem_bytes = static_cast<int64_t>(pr.totalGlobalMem);
+  return CS_OK;
+}
+
+cs_status cs_probe_stream_read(const void* src, size_t bytes, void* sink, cs_stream stream) {
+  if (!src || !sink) return fail(CS_EINVAL, "null src or sink");
+  if (bytes % 16) return fail(CS_EINVAL, "bytes must be a multiple of 16");
+  int dev = 0, cus = 0;
+  CS_HIP(hipGetDevice(&dev), "hipGetDevice");
+  CS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev), "hipDeviceGetAttribute");
+  CS_HIP(cs::launch_stream_read_probe(src, bytes, static_cast<uint32_t*>(sink), cus, as_stream(stream)),
+         "stream read probe launch");
+  return CS_OK;
+}
+
 cs_status cs_profile_start(cs_pool* p) {
   if (!p) return fail(CS_EINVAL, "null pool");
   for (auto& pe : p->prof_events) {

@@ -50,6 +50,11 @@ hipError_t launch_decode_merge_split(const PoolGeom& g, int split_layer, const D
                                      float* split_partials, const float* merge_partials,
                                      void* merge_out, hipStream_t stream);
 
+// Streaming-read probe: read `bytes` (a multiple of 16) of device memory once with non-temporal
+// 16-byte loads on 8 workgroups per CU; `sink` is 4 bytes of device memory (almost never written).
+hipError_t launch_stream_read_probe(const void* src, size_t bytes, uint32_t* sink, int n_cus,
+                                    hipStream_t stream);
+
 // Capacity of the static decode scratch (floats): 16 MiB on each GPU.
 constexpr size_t kStaticScratchFloats = size_t(4) << 20;
 // Device address of the static decode scratch on the current device (looked up once per device
