@@ -1120,6 +1120,40 @@ def bench_mixed(args):
         "spot_parity": parity}}
 
 
+def bench_sim(comps):
+    """The host simulator (paper_2606_01839_amd/sim.py) timed with the rates this run measured
+    (turn-1 prefill curve, decode fixed cost and marginal bandwidth, extend rate, pack/unpack):
+    the 256-conversation agentic trace, Poisson arrivals, 1 prefiller + 2 decoders of 116,000 pages
+    (85% of HBM at 32 layers), 2 s of tool time between turns. CPU only."""
+    from paper_2606_01839_amd.sim import ConvSpec, CostModel, Simulator
+    cost = CostModel.from_bench({"components": comps})
+    convs = MixedTrace().conversations()
+    out = {"workload": "host simulation of the mixed agentic trace (256 conversations) on 1 prefiller + "
+                       "2 decoders, Poisson arrivals, 2 s tool time, rates measured in this run",
+           "cost_model": {k: getattr(cost, k) for k in ("prefill_curve", "decode_fixed_s", "decode_gbs",
+                                                        "extend_tflops", "move_gbs", "link_gbs")}}
+    for rate in (0.2, 1.0):
+        arr = np.cumsum(np.random.default_rng(7).exponential(1.0 / rate, size=len(convs)))
+        spec = [ConvSpec(c.turn1, c.appends, c.decodes, float(a)) for c, a in zip(convs, arr)]
+        sim = Simulator(spec, cost, n_decoders=2, pages_per_decoder=116_000, max_wait_s=30.0, tool_s=2.0)
+        r = sim.run()
+        L = np.array([x[0] for x in r["turn1_ttft"]], dtype=float)
+        T = np.array([x[1] for x in r["turn1_ttft"]])
+        c = np.polyfit(L, T, 2)
+        later = np.array([t for _, _, t in r["later_ttft"]])
+        out[f"rate_{rate}"] = {
+            "completed": r["completed"], "refusals": r["refusals"], "swaps": r["swaps"],
+            "makespan_s": r["makespan_s"], "tokens_per_s": r["tokens_per_s"],
+            "decode_tokens_per_s": r["decode_tokens_per_s"],
+            "turn1_ttft_s_p50_p95": [float(np.median(T)), float(np.percentile(T, 95))],
+            "turn1_ttft_quadratic_r2": float(1 - ((T - np.polyval(c, L)) ** 2).sum() / ((T - T.mean()) ** 2).sum()),
+            "later_ttft_s_p50_p95": [float(np.median(later)), float(np.percentile(later, 95))],
+            "decode_dominated_share_by_active_kv": [
+                {"active_tokens": [lo, hi], "iterations": n, "share": s_}
+                for lo, hi, n, s_ in sim.decode_dominance([0, 131072, 262144, 524288, 1048576, 1 << 40]) if n]}
+    return {"sim": out}
+
+
 def copy_calibration():
     """A plain 1 GiB device copy: its FETCH_SIZE / WRITE_SIZE counters calibrate the HBM traffic
     reported for the decode kernel (known 1 GiB read + 1 GiB written)."""
@@ -1178,6 +1212,7 @@ def main():
         comps.update(bench_decode_curve(args))
         if args.mixed_steps > 0:
             comps.update(bench_mixed(args))
+        comps.update(bench_sim(comps))
     split_gbs = dec["split_bytes"] / (dec["split_ms"] * 1e-3) / 1e9
     line = {
         "metric": METRIC,

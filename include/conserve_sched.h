@@ -69,8 +69,12 @@ typedef struct cs_sched cs_sched;  /* opaque */
 /*
  * Scheduler over n_decoders decoder pools (created by the caller with conserve_attn.h; the
  * scheduler only reads their occupancy and never owns them). max_wait_s bounds the expected wait
- * of a new conversation's turn-1 prefill behind the prefiller's admitted work.
- * Errors: CS_EINVAL (null curve/pools/out, n_decoders < 1, max_wait_s < 0 or not finite).
+ * of a new conversation's turn-1 prefill behind the prefiller's admitted work. n_decoders = 0
+ * (decoders may then be null) makes an admission-only scheduler, for callers that keep decoder
+ * occupancy themselves and bind with cs_place_least_occupied (e.g. a host simulation);
+ * cs_sched_bind on it fails with CS_EINVAL.
+ * Errors: CS_EINVAL (null curve/out, null pools with n_decoders > 0, n_decoders < 0, max_wait_s
+ * < 0 or not finite).
  */
 cs_status cs_sched_create(const cs_prefill_curve* curve, double max_wait_s, int32_t n_decoders,
                           cs_pool* const* decoders, cs_sched** out);

@@ -452,10 +452,11 @@ class Scheduler:
     """Reactive conversation placement over decoder KVPools (cs_sched_*). The pools stay owned
     by the caller and must outlive the scheduler."""
 
-    def __init__(self, coef, max_wait_s: float, decoders):
+    def __init__(self, coef, max_wait_s: float, decoders=()):
+        """decoders = () makes an admission-only scheduler (bind() then raises CS_EINVAL)."""
         self.lib = load_library()
         self.decoders = list(decoders)
-        arr = (ctypes.c_void_p * len(self.decoders))(*[d._handle for d in self.decoders])
+        arr = (ctypes.c_void_p * max(1, len(self.decoders)))(*[d._handle for d in self.decoders])
         c = PrefillCurve(*coef)
         h = ctypes.c_void_p()
         _check(self.lib.cs_sched_create(ctypes.byref(c), float(max_wait_s), len(self.decoders),

@@ -28,8 +28,9 @@ bool fit_prefill_curve(const int64_t* tokens, const double* seconds, int n, Pref
 // Section 4.1: the prefiller saturates at R* = T_p / L_in conversations per second; N decoders
 // must satisfy N T_d >= R* L_d (throughput) and N B >= R* W (memory: B conversations fit on one
 // decoder, each lives W seconds). n_throughput = R* L_d / T_d, n_memory = R* W / B, and the
-// provisioned N is the smallest integer strictly greater than both ("an integer more than
-// satisfying both inequalities"). Returns false for non-positive or non-finite inputs.
+// provisioned N is the smallest integer strictly greater than both (the reading adopted for the
+// section's rule that N exceeds what both inequalities require). Returns false for non-positive or
+// non-finite inputs.
 struct Provisioning {
   double saturation_rate = 0;  // R*
   double n_throughput = 0;

@@ -74,8 +74,9 @@ cs_status cs_place_least_occupied(int32_t n, const int64_t* used_pages, const in
 
 cs_status cs_sched_create(const cs_prefill_curve* curve, double max_wait_s, int32_t n_decoders,
                           cs_pool* const* decoders, cs_sched** out) {
-  if (!curve || !decoders || !out) return cs::api_fail(CS_EINVAL, "null argument");
-  if (n_decoders < 1) return cs::api_fail(CS_EINVAL, "n_decoders < 1");
+  if (!curve || !out) return cs::api_fail(CS_EINVAL, "null argument");
+  if (n_decoders < 0) return cs::api_fail(CS_EINVAL, "n_decoders < 0");
+  if (n_decoders > 0 && !decoders) return cs::api_fail(CS_EINVAL, "null decoder array");
   if (!(max_wait_s >= 0) || !std::isfinite(max_wait_s))
     return cs::api_fail(CS_EINVAL, "max_wait_s must be finite and >= 0");
   for (int32_t i = 0; i < n_decoders; ++i)
@@ -86,7 +87,7 @@ cs_status cs_sched_create(const cs_prefill_curve* curve, double max_wait_s, int3
   c.c2 = curve->c2;
   cs_sched* s = new (std::nothrow) cs_sched(c, max_wait_s);
   if (!s) return cs::api_fail(CS_ENOMEM, "out of host memory");
-  s->decoders.assign(decoders, decoders + n_decoders);
+  if (n_decoders > 0) s->decoders.assign(decoders, decoders + n_decoders);
   *out = s;
   return CS_OK;
 }
@@ -111,6 +112,7 @@ cs_status cs_sched_bind(cs_sched* sched, int64_t kv_tokens, int32_t* decoder) {
   if (!sched || !decoder) return cs::api_fail(CS_EINVAL, "null argument");
   if (kv_tokens < 1) return cs::api_fail(CS_EINVAL, "kv_tokens < 1");
   const int32_t n = static_cast<int32_t>(sched->decoders.size());
+  if (n == 0) return cs::api_fail(CS_EINVAL, "the scheduler has no decoder pools (admission only)");
   std::vector<int64_t> used(n), free_(n);
   for (int32_t i = 0; i < n; ++i) {
     const cs_status st = cs_pool_occupancy(sched->decoders[i], &used[i], &free_[i]);

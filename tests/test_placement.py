@@ -206,3 +206,22 @@ def test_scheduler_binds_by_capacity_and_validates():
     s.close()
     small.close()
     large.close()
+
+
+def test_admission_only_scheduler():
+    """n_decoders = 0: admission works (the same decisions as the oracle), bind is refused."""
+    import paper_2606_01839_amd as m
+    from paper_2606_01839_amd import ConserveError, CS_EINVAL
+    coef = (0.002, 3e-6, 2e-11)
+    s = m.Scheduler(coef, 0.05)
+    o = op.Admission(coef, 0.05)
+    rng = np.random.default_rng(15)
+    now = 0.0
+    for _ in range(200):
+        now += float(rng.exponential(0.02))
+        L = int(rng.integers(1, 40000))
+        assert s.admit(L, now) == o.admit(L, now)
+    with pytest.raises(ConserveError) as e:
+        s.bind(16)
+    assert e.value.code == CS_EINVAL
+    s.close()
