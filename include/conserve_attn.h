@@ -23,8 +23,10 @@
  *    scale is exactly 1/sqrt(head_dim). Query head h reads KV head h / (n_q_heads / n_kv_heads).
  *  - Errors: every call validates all arguments before changing any state; on error it returns a
  *    negative cs_status, changes nothing, and sets a thread-local message (cs_last_error). Nothing
- *    aborts or throws across this ABI. CS_EHIP reports a failing HIP runtime call; the pool may then
- *    be inconsistent with the device and should be destroyed.
+ *    aborts or throws across this ABI. CS_EHIP reports a failing HIP runtime call; an append that
+ *    fails so still changes no length and no page (its reserved pages return to the free list);
+ *    cs_mixed_step's append is complete when a later attention launch fails; after any CS_EHIP
+ *    the outputs of the failing call are undefined.
  *  - Asynchrony: host metadata (lengths, page tables) is committed when the call returns; kernels
  *    and the small metadata uploads they need are enqueued on `stream` (a hipStream_t, 0 = null
  *    stream). No call synchronises the device, except that switching a pool to another stream
@@ -292,6 +294,14 @@ cs_status cs_device_info(int32_t device, cs_device_info_t* out);
  * Errors: CS_EINVAL (null pointers, bytes not a multiple of 16), CS_EHIP.
  */
 cs_status cs_probe_stream_read(const void* src, size_t bytes, void* sink, cs_stream stream);
+
+/*
+ * Test instrumentation of the error paths: after `after` more kernel launches of this pool
+ * succeed, every later launch of the pool reports CS_EHIP ("failure injected") without launching
+ * anything, until the call is made again with after < 0 (off, the default). The failing call
+ * behaves as on a real HIP launch failure at that point. Errors: CS_EINVAL (null pool).
+ */
+cs_status cs_debug_fail_launches(cs_pool* pool, int64_t after);
 
 /* Message of the last failing call on this thread ("" if none). Valid until the next call. */
 const char* cs_last_error(void);

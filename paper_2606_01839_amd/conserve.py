@@ -28,7 +28,8 @@ EXPORTS = [
     "cs_kv_append", "cs_kv_append_batch", "cs_attn_prefill_turn1", "cs_attn_extend",
     "cs_attn_decode_batch", "cs_attn_decode_batch_noalloc", "cs_mixed_step", "cs_kv_pack_size", "cs_kv_pack", "cs_kv_unpack",
     "cs_profile_start",
-    "cs_profile_stop", "cs_device_info", "cs_probe_stream_read", "cs_last_error",
+    "cs_profile_stop", "cs_device_info", "cs_probe_stream_read", "cs_debug_fail_launches",
+    "cs_last_error",
     # placement layer (include/conserve_sched.h)
     "cs_prefill_curve_fit", "cs_prefill_curve_eval", "cs_provision_decoders",
     "cs_place_least_occupied", "cs_sched_create", "cs_sched_destroy", "cs_sched_admit",
@@ -100,6 +101,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "cs_profile_start": (I32, [P]),
         "cs_profile_stop": (I32, [P, ctypes.POINTER(ctypes.c_double), PI64]),
         "cs_device_info": (I32, [I32, ctypes.POINTER(DeviceInfo)]),
+        "cs_debug_fail_launches": (I32, [P, I64]),
         "cs_probe_stream_read": (I32, [VP, SZ, VP, VP]),
         "cs_last_error": (ctypes.c_char_p, []),
         "cs_prefill_curve_fit": (I32, [I32, PI64, ctypes.POINTER(ctypes.c_double),
@@ -333,6 +335,10 @@ class KVPool:
         return out_ext, out_dec
 
     # -- instrumentation -----------------------------------------------------------------------
+    def debug_fail_launches(self, after: int) -> None:
+        """cs_debug_fail_launches: launches after the next `after` report CS_EHIP (after < 0: off)."""
+        _check(self.lib.cs_debug_fail_launches(self._handle, int(after)))
+
     def profile_start(self) -> None:
         _check(self.lib.cs_profile_start(self._handle))
 

@@ -110,6 +110,7 @@ struct cs_pool {
     int launches;
   };
   bool prof_on = false;
+  int64_t fail_after = -1;  // cs_debug_fail_launches: launches left before the injected failure
   // an open span: one pair of events brackets a run of launches of one kind on one stream
   bool span_open = false;
   hipEvent_t span_start = nullptr;
@@ -200,6 +201,8 @@ hipError_t take_event(cs_pool* p, hipEvent_t* e) {
 // (inside an open span the span's events cover it and it only counts as one more launch).
 template <typename F>
 cs_status timed_launch_on(cs_pool* p, hipStream_t s, int kind, const char* what, F&& launch) {
+  if (p->fail_after == 0) return fail(CS_EHIP, std::string(what) + ": failure injected by cs_debug_fail_launches");
+  if (p->fail_after > 0) --p->fail_after;
   if (p->prof_on && p->span_open) {
     CS_HIP(launch(), what);
     ++p->span_launches;
@@ -505,32 +508,52 @@ cs_status append_impl(cs_pool* p, int32_t n, const cs_conv* convs, const int32_t
   if ((st = ensure_device(p)) != CS_OK) return st;
   if ((st = use_stream(p, as_stream(stream))) != CS_OK) return st;
 
-  // Commit host metadata: reserve pages (cannot fail now), build chunks, update lengths.
+  // Reserve pages (cannot fail now) and build the chunks; lengths are committed only after every
+  // upload and launch has been issued. If one of those fails, the reserved pages go back to the
+  // free list in their old order and nothing about the conversations changes. (Launches already
+  // issued may have written the new tokens into the reserved pages and into unused slots past a
+  // conversation's end; no kernel reads those: attention masks keys past the length, pack writes
+  // zeros there, and the pages return to the free list.)
   std::vector<int32_t> slots(n), nn(n_new, n_new + n);
   std::vector<int64_t> old_lens(n);
+  std::vector<size_t> old_pages(n);
   std::vector<const std::vector<int32_t>*> lists(n);
   for (int32_t i = 0; i < n; ++i) {
     cs::Conv* c = p->convs.find(convs[i]);
     slots[i] = cs::ConvTable::slot_of(convs[i]);
     old_lens[i] = c->len;
+    old_pages[i] = c->pages.size();
     p->pages.alloc(cs::pages_for(c->len + n_new[i]) - cs::pages_for(c->len), c->pages);
     lists[i] = &c->pages;
   }
   std::vector<cs::PageChunk> chunks = cs::plan_append(slots, old_lens, nn, lists);
-  for (int32_t i = 0; i < n; ++i) p->convs.find(convs[i])->len += n_new[i];
+  auto roll_back = [&] {
+    std::vector<int32_t> taken;
+    for (int32_t i = 0; i < n; ++i) {
+      cs::Conv* c = p->convs.find(convs[i]);
+      taken.insert(taken.end(), c->pages.begin() + static_cast<std::ptrdiff_t>(old_pages[i]), c->pages.end());
+      c->pages.resize(old_pages[i]);
+    }
+    p->pages.unalloc(taken);
+  };
 
   const cs::PoolGeom g = p->geom();
   const size_t per = kQuarter / sizeof(cs::PageChunk) - 1;
   for (size_t c0 = 0; c0 < chunks.size(); c0 += per) {
     const size_t c1 = std::min(chunks.size(), c0 + per);
     void* d = nullptr;
-    if ((st = upload(p, chunks.data() + c0, (c1 - c0) * sizeof(cs::PageChunk), &d)) != CS_OK) return st;
-    st = timed_launch(p, CS_PROF_APPEND, "append launch", [&] {
-      return cs::launch_append(g, static_cast<const cs::PageChunk*>(d), static_cast<int>(c1 - c0), k, v,
-                               total, p->stream);
-    });
-    if (st != CS_OK) return st;
+    st = upload(p, chunks.data() + c0, (c1 - c0) * sizeof(cs::PageChunk), &d);
+    if (st == CS_OK)
+      st = timed_launch(p, CS_PROF_APPEND, "append launch", [&] {
+        return cs::launch_append(g, static_cast<const cs::PageChunk*>(d), static_cast<int>(c1 - c0), k, v,
+                                 total, p->stream);
+      });
+    if (st != CS_OK) {
+      roll_back();
+      return st;
+    }
   }
+  for (int32_t i = 0; i < n; ++i) p->convs.find(convs[i])->len += n_new[i];
   return CS_OK;
 }
 
@@ -971,6 +994,12 @@ cs_status cs_probe_stream_read(const void* src, size_t bytes, void* sink, cs_str
   CS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev), "hipDeviceGetAttribute");
   CS_HIP(cs::launch_stream_read_probe(src, bytes, static_cast<uint32_t*>(sink), cus, as_stream(stream)),
          "stream read probe launch");
+  return CS_OK;
+}
+
+cs_status cs_debug_fail_launches(cs_pool* p, int64_t after) {
+  if (!p) return fail(CS_EINVAL, "null pool");
+  p->fail_after = after < 0 ? -1 : after;
   return CS_OK;
 }
 

@@ -34,6 +34,10 @@ void PagePool::release(const std::vector<int32_t>& pages) {
   }
 }
 
+void PagePool::unalloc(const std::vector<int32_t>& pages) {
+  for (auto it = pages.rbegin(); it != pages.rend(); ++it) free_.push_back(*it);
+}
+
 ConvTable::ConvTable(int32_t max_convs, int32_t max_pages_per_conv)
     : max_convs_(max_convs), max_pages_(max_pages_per_conv), slots_(static_cast<size_t>(max_convs)) {
   for (int32_t i = 0; i < max_convs; ++i) free_slots_.push_back(i);

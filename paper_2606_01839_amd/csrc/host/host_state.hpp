@@ -37,6 +37,9 @@ class PagePool {
   // All-or-nothing: appends n page ids to `out` and returns true, or changes nothing.
   bool alloc(int64_t n, std::vector<int32_t>& out);
   void release(const std::vector<int32_t>& pages);
+  // Undo the latest alloc calls exactly: `pages` are the ids they handed out, in order (the free
+  // list then holds the same ids in the same order as before them).
+  void unalloc(const std::vector<int32_t>& pages);
 
  private:
   int64_t n_pages_;

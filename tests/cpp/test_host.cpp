@@ -34,6 +34,12 @@ static void pool_basics() {
   CHECK(a.free_count() == 10);
   CHECK(!a.alloc(11, more) && more.empty());
   CHECK(a.alloc(10, more) && more.size() == 10);
+  // unalloc undoes allocations exactly: the next allocations hand out the same ids again
+  cs::PagePool u(50, 3), w(50, 3);
+  std::vector<int32_t> u1, u2, w1;
+  CHECK(u.alloc(7, u1) && u.alloc(5, u1));
+  u.unalloc(u1);
+  CHECK(u.free_count() == 50 && u.alloc(20, u2) && w.alloc(20, w1) && u2 == w1);
 }
 
 static void conv_table() {
