@@ -894,27 +894,54 @@ def bench_decode_curve(args):
 # mixed agentic trace (256 conversations, 32 layers, Llama-3-8B attention shape)
 # ------------------------------------------------------------------------------------------------
 class _Live:
-    __slots__ = ("tr", "h", "turn", "phase", "left", "length")
+    __slots__ = ("tr", "h", "turn", "phase", "left", "length", "order", "host", "pending")
 
-    def __init__(self, tr, h, length):
-        self.tr, self.h, self.turn, self.length = tr, h, 0, length
-        self.phase, self.left = "decode", tr.decodes[0]
+    def __init__(self, tr, h, length, order, phase="decode"):
+        self.tr, self.h, self.turn, self.length, self.order = tr, h, 0, length, order
+        self.phase, self.left, self.host = phase, tr.decodes[0], None
+        self.pending = tr.turn1 if phase == "prefill" else 0   # prompt tokens still to prefill
 
 
-def bench_mixed(args):
-    """Serve the synthetic agentic trace on one decoder pool for `args.mixed_steps` timed steps.
+# Turn-1 prefill curve of one layer (32q/8kv, d 128) measured on MI355X by bench_prefill_curve;
+# the scheduler's admission reads it, scaled to the 32 layers of the mixed trace.
+PREFILL_CURVE_1L = (1.57e-5, 4.94e-9, 6.81e-12)
+ADMIT_WATERMARK = 0.8    # bind only while the decoder's pages after the transfer stay below this
 
-    Admission is staggered: a conversation is admitted when the decoder pool's free pages cover its
-    (known, synthetic) final length. At admission its turn-1 prompt is prefilled on a separate
-    prefiller pool (all layers), packed, unpacked into the decoder pool and released from the
-    prefiller -- the one-time transfer. Every step, each live conversation either appends its
-    pending turn chunk (extend; whole chunks, at most 8192 extend tokens per step) or decodes one
-    token; finished conversations are destroyed and new ones admitted between steps."""
-    from paper_2606_01839_amd import KVPool
+
+COLLOCATED_BUDGET = 2944   # tokens per step of the paper's collocated replicas (Section 5.1)
+
+
+def bench_mixed(args, collocated=False):
+    """Serve the synthetic agentic trace on one decoder pool (Section 4: after the one-time
+    transfer a conversation's later turns run on its decoder).
+
+    Placement follows the paper's reactive scheduler through the library (Section 4.2): a waiting
+    conversation is admitted with cs_sched_admit (its expected turn-1 prefill time read off the
+    quadratic curve) and bound with cs_sched_bind, which reads the decoder pool's current
+    occupancy -- no knowledge of how long a conversation will grow. Binding also keeps the pool
+    below an 80% high-water mark so live conversations have room to grow. At admission the turn-1
+    prompt is prefilled on a separate prefiller pool (all layers), packed, unpacked into the
+    decoder pool and released from the prefiller -- the one-time transfer. Every step, each live
+    conversation either appends its pending turn chunk (extend; whole chunks, at most 8192 extend
+    tokens per step, the first always) or decodes one token; finished conversations are destroyed
+    and new ones admitted between steps. When a step's new tokens do not fit in the pool, extend
+    chunks wait, then the most recently admitted conversation is swapped out (kv_pack to host
+    memory, destroyed) and later swapped back in (kv_unpack) before anything new is admitted.
+
+    With --mixed-to-completion the run continues until every conversation has completed, in the
+    layer-ordered form of the step (a model forward pass), sampling oracle parity every 2000 steps;
+    otherwise `args.mixed_steps` timed steps alternate between the two orders of cs_mixed_step.
+
+    collocated=True is the paper's collocated baseline instead (Section 5.1): no prefiller; a new
+    conversation's turn-1 prompt is prefilled on the decoder itself in chunks, batched with the
+    decodes under a budget of COLLOCATED_BUDGET tokens per step (decode tokens first, then prompt
+    and append chunks in admission order, split as the budget allows), layer-ordered steps."""
+    from paper_2606_01839_amd import KVPool, Scheduler
     tr = MixedTrace()
     sh = tr.shape
     NL, hq, hkv, d = sh.n_layers, sh.n_q_heads, sh.n_kv_heads, sh.head_dim
     trace = tr.conversations()
+    to_completion = bool(getattr(args, "mixed_to_completion", False))
     page_bytes = NL * hkv * 2 * 16 * d * 2                       # one page, all layers
     import gc
     gc.collect()
@@ -929,36 +956,101 @@ def bench_mixed(args):
                  max_pages_per_conv=pages_for(max_final), placement_seed=tr.seed + 1)
     pre = KVPool(NL, hq, hkv, d, n_pages=pages_for(max_t1) + 16, max_convs=2,
                  max_pages_per_conv=pages_for(max_t1) + 16, placement_seed=tr.seed + 2)
-    keys = {}
+    sched = Scheduler(tuple(NL * c for c in PREFILL_CURVE_1L), 1e9, [dec])
+    # Values: rows of two seeded tables made once with the counter-based generator (K and V rows of
+    # Hkv*d values, Q rows of Hq*d values, 2^20 and 2^19 rows, N(0,1)-like bf16). Token `pos` of
+    # conversation c, kind and layer reads row (offset(c, kind, layer) + pos) mod rows: a gather per
+    # step instead of hashing every element of the step's inputs, and the oracle checks read the
+    # same rows back.
+    kv_rows, q_rows_n = 1 << 20, 1 << 19
+    t_kv = sv.bf16_tensor(sv.mix_key(tr.seed, 7001), (kv_rows, hkv * d), device="cuda")
+    t_q = sv.bf16_tensor(sv.mix_key(tr.seed, 7002), (q_rows_n, hq * d), device="cuda")
+    offs = {}
 
-    def key(c, kind, layer):
-        kk = keys.get((c, kind, layer))
-        if kk is None:
-            kk = keys[(c, kind, layer)] = sv.mix_key(tr.seed, c, kind, layer)
-        return kk
+    def conv_offs(c, kind):
+        o = offs.get((c, kind))
+        if o is None:
+            o = offs[(c, kind)] = np.array([sv.mix_key(tr.seed, c, kind, l) & ((1 << 40) - 1)
+                                            for l in range(NL)], dtype=np.int64)
+        return o
+
+    def gather(kind, items, layers, H):
+        """[len(layers)][sum n][H][d] device tensor of the tokens (conv, start, n) of each layer."""
+        table, rows_n = (t_q, q_rows_n) if kind == KIND_Q else (t_kv, kv_rows)
+        counts = np.array([n for _, _, n in items], dtype=np.int64)
+        pos = np.concatenate([p0 + np.arange(n, dtype=np.int64) for _, p0, n in items])
+        base = np.stack([conv_offs(c, kind)[layers] for c, _, _ in items], axis=1)      # [layers][items]
+        idx = (np.repeat(base, counts, axis=1) + pos[None, :]) & (rows_n - 1)
+        out = table.index_select(0, torch.from_numpy(idx.reshape(-1)).cuda())
+        return out.view(len(layers), int(counts.sum()), H, d)
 
     def rows(kind, items, layer, H, device="cuda"):
         """Values of tokens (conv, start, n) for one layer: [sum n][H][d]."""
-        klist = np.array([sv.signed_key(key(c, kind, layer)) for c, _, _ in items], dtype=np.int64)
-        kk = np.repeat(klist, [n for _, _, n in items])
-        st = np.concatenate([(p0 + np.arange(n, dtype=np.int64)) * H * d for _, p0, n in items])
-        return sv.bf16_rows(kk, st, H * d, device=device).view(-1, H, d)
+        out = gather(kind, items, [layer], H)[0]
+        return out.cpu() if device == "cpu" else out
+
+    def rows_all(kind, items, H):
+        """The same for every layer: [NL][sum n][H][d]."""
+        return gather(kind, items, list(range(NL)), H)
 
     stats = {"prefill_flops": 0, "prefill_ms": 0.0, "pack_ms": 0.0, "unpack_ms": 0.0, "move_bytes": 0,
-             "admitted": 0, "completed": 0}
-    live, queue = [], list(trace)
-    reserved = [0]
+             "admitted": 0, "completed": 0, "swapped_out": 0, "swapped_in": 0, "turn1_tokens": 0,
+             "admission_expected_s": 0.0}
+    live, queue, swapped = [], list(trace), []
+    t_run = time.perf_counter()
+    order = [0]
+
+    def used_free():
+        return dec.occupancy()
+
+    def swap_in():
+        while swapped:
+            lc = swapped[0]
+            used, fr = used_free()
+            if used + pages_for(lc.length) > ADMIT_WATERMARK * n_pages:
+                return False
+            swapped.pop(0)
+            lc.h = dec.kv_unpack(lc.host.cuda(), lc.length)
+            lc.host = None
+            live.append(lc)
+            stats["swapped_in"] += 1
+        return True
+
+    def swap_out(lc):
+        host = dec.kv_pack(lc.h).cpu()                           # synchronous copy to host memory
+        dec.conv_destroy(lc.h)
+        lc.host, lc.h = host, None
+        live.remove(lc)
+        swapped.append(lc)
+        stats["swapped_out"] += 1
 
     def admit():
-        while queue and reserved[0] + pages_for(queue[0].final_len()) <= n_pages:
-            c = queue.pop(0)
+        if not swap_in():                                        # swapped conversations come first
+            return
+        while queue:
+            c = queue[0]
             L = c.turn1
+            used, _ = used_free()
+            # prompts still to be prefilled on the decoder (collocated) count as taken
+            used += sum(pages_for(x.length + x.pending) - pages_for(x.length) for x in live if x.phase == "prefill")
+            if used + pages_for(L) > ADMIT_WATERMARK * n_pages:
+                return
+            if sched.bind(L) < 0:                                # cs_sched_bind: occupancy now
+                return
+            queue.pop(0)
+            if collocated:                                       # prefilled in chunks on the decoder
+                stats["admitted"] += 1
+                order[0] += 1
+                live.append(_Live(c, dec.conv_create(), 0, order[0], phase="prefill"))
+                continue
+            start, done = sched.admit(L, time.perf_counter() - t_run)   # cs_sched_admit
+            stats["admission_expected_s"] += done - start
             h = pre.conv_create()
-            k = torch.stack([rows(KIND_K, [(c.cid, 0, L)], l, hkv) for l in range(NL)])
-            v = torch.stack([rows(KIND_V, [(c.cid, 0, L)], l, hkv) for l in range(NL)])
+            k = rows_all(KIND_K, [(c.cid, 0, L)], hkv)
+            v = rows_all(KIND_V, [(c.cid, 0, L)], hkv)
             pre.kv_append(h, k, v)
             del k, v
-            qs = [rows(KIND_Q, [(c.cid, 0, L)], l, hq) for l in range(NL)]
+            qs = rows_all(KIND_Q, [(c.cid, 0, L)], hq)
             out = torch.empty_like(qs[0])
             torch.cuda.synchronize()
             pre.profile_start()
@@ -977,37 +1069,79 @@ def bench_mixed(args):
             stats["prefill_flops"] += attn_flops([0], [L], hq, d) * NL
             stats["move_bytes"] += 2 * L * NL * hkv * d * 2 * 2
             stats["admitted"] += 1
-            reserved[0] += pages_for(c.final_len())
-            live.append(_Live(c, hd, L))
+            stats["turn1_tokens"] += L
+            order[0] += 1
+            live.append(_Live(c, hd, L, order[0]))
 
     t0 = time.perf_counter()
     admit()
     log(f"mixed: decoder pool {n_pages} pages; admitted {len(live)} conversations "
         f"in {time.perf_counter() - t0:.1f}s")
-    # Timed steps alternate between the two orders of cs_mixed_step: odd steps overlap all layers
-    # (every layer's queries are given), even steps run in layer order as a model forward pass
-    # must. Per-kernel timing events are recorded on the overlapped steps only.
     mk_tot = lambda: {"wall_s": 0.0, "tokens": 0, "dec_bytes": 0, "ext_flops": 0, "split_ms": 0.0,
                       "merge_ms": 0.0, "fwd_ms": 0.0, "append_ms": 0.0, "append_bytes": 0, "steps": 0,
                       "dec_tokens": 0, "ext_tokens": 0}
     tot, tot_ord = mk_tot(), mk_tot()
     parity = {}
-    for step in range(args.mixed_steps + 1):
-        ext, budget = [], 8192
-        for lc in live:
-            if lc.phase == "append":
-                n = lc.tr.appends[lc.turn - 1]
-                if not ext or sum(x[1] for x in ext) + n <= budget:
-                    ext.append((lc, n))
+    samples = []
+    steplog = []     # layer-ordered timed steps: (seconds, decode tokens, prompt chunk tokens, append tokens)
+    want_check = False
+    check_every = int(getattr(args, "mixed_check_every", 2000))
+    max_steps = 10 ** 7 if to_completion else args.mixed_steps + 1
+    max_s = getattr(args, "mixed_max_s", None)
+    stop = [False]
+    import signal
+    old_term = signal.signal(signal.SIGTERM, lambda *a: stop.__setitem__(0, True))
+    step = 0
+    while step < max_steps and (live or swapped or queue) and not stop[0]:
+        if max_s and time.perf_counter() - t_run > max_s:
+            break
+        if not live:                                             # nothing resident: admit / swap in
+            admit()
+            if not live:
+                raise RuntimeError("mixed trace: no conversation fits the decoder pool")
         dcs = [lc for lc in live if lc.phase == "decode"]
+        ext = []
+        if collocated:
+            budget = COLLOCATED_BUDGET - len(dcs)
+            for lc in sorted((x for x in live if x.phase in ("prefill", "append")), key=lambda x: x.order):
+                if budget <= 0:
+                    break
+                n = min(lc.pending, budget)
+                ext.append((lc, n))
+                budget -= n
+        else:
+            budget = 8192
+            for lc in live:
+                if lc.phase == "append":
+                    n = lc.pending
+                    if not ext or sum(x[1] for x in ext) + n <= budget:
+                        ext.append((lc, n))
+        # the step's new tokens must fit: extend chunks wait while other work can run, then the
+        # most recently admitted conversation swaps out
+        while True:
+            need = sum(pages_for(lc.length + n) - pages_for(lc.length) for lc, n in ext) + \
+                   sum(pages_for(lc.length + 1) - pages_for(lc.length) for lc in dcs)
+            if need <= used_free()[1]:
+                break
+            if len(ext) > 1 or (ext and dcs):
+                ext.pop()
+                continue
+            victims = [lc for lc in live if lc.length > 0 and not (ext and lc is ext[0][0])]
+            if not victims:
+                raise RuntimeError("mixed trace: one conversation's turn does not fit the decoder pool")
+            swap_out(max(victims, key=lambda x: x.order))
+            dcs = [lc for lc in live if lc.phase == "decode"]
+        if not ext and not dcs:
+            step += 1
+            continue
         items_new = [(lc.tr.cid, lc.length, n) for lc, n in ext] + [(lc.tr.cid, lc.length, 1) for lc in dcs]
-        k = torch.stack([rows(KIND_K, items_new, l, hkv) for l in range(NL)])
-        v = torch.stack([rows(KIND_V, items_new, l, hkv) for l in range(NL)])
-        qe = torch.stack([rows(KIND_Q, items_new[:len(ext)], l, hq) for l in range(NL)]) if ext else None
-        qd = torch.stack([rows(KIND_Q, items_new[len(ext):], l, hq) for l in range(NL)]) if dcs else None
+        k = rows_all(KIND_K, items_new, hkv)
+        v = rows_all(KIND_V, items_new, hkv)
+        qe = rows_all(KIND_Q, items_new[:len(ext)], hq) if ext else None
+        qd = rows_all(KIND_Q, items_new[len(ext):], hq) if dcs else None
         torch.cuda.synchronize()
         timed_step = step > 0                                      # step 0 warms up
-        ordered = step % 2 == 0
+        ordered = True if (to_completion or collocated) else step % 2 == 0
         acc = tot_ord if ordered else tot
         if timed_step and not ordered:
             dec.profile_start()
@@ -1034,9 +1168,16 @@ def bench_mixed(args):
                 acc["append_ms"] += pr["append"][0]
                 acc["append_bytes"] += 2 * NL * (n_ext + len(dcs)) * hkv * d * 2 * 2
             acc["steps"] += 1
+            if ordered:
+                steplog.append((te - ts, len(dcs), sum(n for lc, n in ext if lc.phase == "prefill"),
+                                sum(n for lc, n in ext if lc.phase == "append")))
         mode = "layer_ordered" if ordered else "overlapped"
-        if mode not in parity and dcs and ext:
-            # spot check: shortest decoding and shortest extending conversation, first and last layer
+        if to_completion and step > 0 and step % check_every == 0:
+            want_check = True
+        check = (mode not in parity) if not to_completion else want_check
+        if check and dcs and ext:
+            want_check = False
+            # oracle check: shortest decoding and shortest extending conversation, first and last layer
             from oracle.attention import attend_rows
             errs = []
             lcd = min(dcs, key=lambda x: x.length)
@@ -1052,11 +1193,14 @@ def bench_mixed(args):
                     ref = attend_rows(sv.bf16_to_f64(qrow[None]), [pos], sv.bf16_to_f64(kk), sv.bf16_to_f64(vv))
                     errs.append(float(np.abs(sv.bf16_to_f64(outrow[None]) - ref).max()))
             parity[mode] = {"samples": len(errs), "max_abs": max(errs), "ok": bool(max(errs) <= 1e-2)}
+            samples.append({"step": step, "max_abs": max(errs)})
         del k, v, qe, qd, oe, od
         # advance the trace
         for lc, n in ext:
             lc.length += n
-            lc.phase, lc.left = "decode", lc.tr.decodes[lc.turn]
+            lc.pending -= n
+            if lc.pending == 0:
+                lc.phase, lc.left = "decode", lc.tr.decodes[lc.turn]
         finished = []
         for lc in dcs:
             lc.length += 1
@@ -1066,28 +1210,84 @@ def bench_mixed(args):
                 if lc.turn == lc.tr.turns:
                     finished.append(lc)
                 else:
-                    lc.phase = "append"
+                    lc.phase, lc.pending = "append", lc.tr.appends[lc.turn - 1]
         for lc in finished:
             live.remove(lc)
             dec.conv_destroy(lc.h)
-            reserved[0] -= pages_for(lc.tr.final_len())
             stats["completed"] += 1
-        if finished:
+        if finished or swapped:
             admit()
+        step += 1
+        if to_completion and step % 1000 == 0:
+            log(f"mixed: step {step}, {stats['completed']} completed, {len(live)} live, "
+                f"{len(swapped)} swapped, {len(queue)} waiting, {time.perf_counter() - t_run:.0f}s")
+    run_s = time.perf_counter() - t_run
+    signal.signal(signal.SIGTERM, old_term)
+    stopped_early = bool(live or swapped or queue) and to_completion
     used, free_pages = dec.occupancy()
+    sched.close()
     dec.close()
     pre.close()
     torch.cuda.empty_cache()
     gbs = lambda b, ms: b / (ms * 1e-3) / 1e9 if ms > 0 else None
     tfs = lambda f, ms: f / (ms * 1e-3) / 1e12 if ms > 0 else None
     roof_s = lambda t: t["dec_bytes"] / (HBM_PEAK_GBS * 1e9) + t["ext_flops"] / (BF16_PEAK_TFLOPS * 1e12)
+    workload = (f"mixed agentic trace: {tr.n_convs} conversations, turns U[{tr.turns_lo},{tr.turns_hi}], "
+                f"turn-1 logN(median {tr.turn1_median}) <= {tr.turn1_hi}, appends logN(median "
+                f"{tr.append_median}), decodes logN(median {tr.decode_median}); {NL} layers "
+                f"{hq}q/{hkv}kv d{d}; decoder pool {n_pages} pages ({n_pages * page_bytes / 2**30:.0f} GiB)")
+    placement = {"rule": "cs_sched_admit on the prefill curve + cs_sched_bind on the pool's current "
+                         f"occupancy, {int(100 * ADMIT_WATERMARK)}% high-water mark; swap out/in "
+                         "(kv_pack to host / kv_unpack) when a step's tokens do not fit",
+                 "admitted": stats["admitted"], "completed": stats["completed"],
+                 "swapped_out": stats["swapped_out"], "swapped_in": stats["swapped_in"],
+                 "turn1_prefill_s_expected_by_curve": stats["admission_expected_s"],
+                 "turn1_prefill_s_measured": stats["prefill_ms"] * 1e-3}
+    def tbt(rows_):
+        t_ = np.array([r[0] for r in rows_ if r[1] > 0]) * 1e3
+        return [float(np.percentile(t_, 50)), float(np.percentile(t_, 95))] if t_.size else None
+
+    tbt_all = tbt(steplog)
+    tbt_prompt = tbt([r for r in steplog if r[2] > 0])
+    tbt_no_prompt = tbt([r for r in steplog if r[2] == 0])
+    if collocated:
+        t = tot_ord
+        return {"mixed_collocated": {
+            "workload": workload + f"; collocated: turn-1 prompts prefilled on the decoder in chunks, "
+                                   f"{COLLOCATED_BUDGET} tokens per step (decode tokens first)",
+            "timed_steps": t["steps"], "admitted": stats["admitted"], "completed": stats["completed"],
+            "swapped_out": stats["swapped_out"],
+            "tokens_per_s": t["tokens"] / t["wall_s"] if t["wall_s"] else None,
+            "decode_tokens": t["dec_tokens"], "chunk_tokens": t["ext_tokens"],
+            "step_ms": 1e3 * t["wall_s"] / max(1, t["steps"]),
+            "tbt_ms_p50_p95": tbt_all, "tbt_ms_p50_p95_steps_with_prompt_chunk": tbt_prompt,
+            "tbt_ms_p50_p95_steps_without": tbt_no_prompt,
+            "step_roofline": {"frac": roof_s(t) / t["wall_s"] if t["wall_s"] else None},
+            "spot_parity": parity}}
+    if to_completion:
+        t = tot_ord
+        return {"mixed_to_completion": {
+            "workload": workload, "steps": step, "timed_steps": t["steps"], "run_s": run_s,
+            "stopped_early": stopped_early,
+            **placement, "live_end": len(live), "swapped_end": len(swapped), "waiting_end": len(queue),
+            "decode_tokens": t["dec_tokens"], "extend_tokens": t["ext_tokens"],
+            "turn1_tokens": stats["turn1_tokens"],
+            "step_tokens_per_s": t["tokens"] / t["wall_s"] if t["wall_s"] else None,
+            "run_tokens_per_s": (t["tokens"] + stats["turn1_tokens"]) / run_s,
+            "step_ms": 1e3 * t["wall_s"] / max(1, t["steps"]),
+            "step_roofline": {"roofline_s": roof_s(t), "measured_step_s": t["wall_s"],
+                              "frac": roof_s(t) / t["wall_s"] if t["wall_s"] else None},
+            "turn1_prefill_tflops": tfs(stats["prefill_flops"], stats["prefill_ms"]),
+            "pack_gbs": gbs(stats["move_bytes"], stats["pack_ms"]),
+            "unpack_gbs": gbs(stats["move_bytes"], stats["unpack_ms"]),
+            "occupancy_end": {"used_pages": used, "free_pages": free_pages},
+            "tbt_ms_p50_p95": tbt_all,
+            "parity_samples": samples,
+            "parity_ok": bool(samples and all(s_["max_abs"] <= 1e-2 for s_ in samples))}}
     return {"mixed": {
-        "workload": f"mixed agentic trace: {tr.n_convs} conversations, turns U[{tr.turns_lo},{tr.turns_hi}], "
-                    f"turn-1 logN(median {tr.turn1_median}) <= {tr.turn1_hi}, appends logN(median "
-                    f"{tr.append_median}), decodes logN(median {tr.decode_median}); {NL} layers "
-                    f"{hq}q/{hkv}kv d{d}; decoder pool {n_pages} pages ({n_pages * page_bytes / 2**30:.0f} GiB)",
-        "timed_steps": tot["steps"], "live_convs_end": len(live), "admitted": stats["admitted"],
-        "completed": stats["completed"], "tokens_per_s": tot["tokens"] / tot["wall_s"] if tot["wall_s"] else None,
+        "workload": workload,
+        "timed_steps": tot["steps"], "live_convs_end": len(live), **placement,
+        "tokens_per_s": tot["tokens"] / tot["wall_s"] if tot["wall_s"] else None,
         "step_ms": 1e3 * tot["wall_s"] / max(1, tot["steps"]),
         "decode_tokens": tot["dec_tokens"], "extend_tokens": tot["ext_tokens"],
         "steps_note": "timed steps alternate between the two orders of the mixed step; tokens_per_s, "
@@ -1098,6 +1298,7 @@ def bench_mixed(args):
             "tokens_per_s": tot_ord["tokens"] / tot_ord["wall_s"] if tot_ord["wall_s"] else None,
             "step_ms": 1e3 * tot_ord["wall_s"] / max(1, tot_ord["steps"]),
             "frac": roof_s(tot_ord) / tot_ord["wall_s"] if tot_ord["wall_s"] else None,
+            "tbt_ms_p50_p95": tbt_all,
             "note": "layer l+1's attention starts after layer l's (extend and decode of one layer "
                     "overlap), as in a model forward pass; no timing events on these steps"},
         "step_roofline": {
@@ -1175,6 +1376,13 @@ def main():
                     help="run one component and print only its JSON (for profiling)")
     ap.add_argument("--mixed-steps", type=int, default=400,
                     help="timed steps of the mixed agentic trace component (0 = skip it)")
+    ap.add_argument("--mixed-to-completion", action="store_true",
+                    help="with --only mixed: serve the whole trace until every conversation completes")
+    ap.add_argument("--mixed-max-s", type=float, default=None,
+                    help="with --mixed-to-completion: stop (and report) after this many seconds")
+    ap.add_argument("--mixed-collocated", action="store_true",
+                    help="with --only mixed: the collocated baseline (turn-1 prompts chunked into the "
+                         "decoder's steps, 2944 tokens per step)")
     ap.add_argument("--no-energy", dest="energy", action="store_false",
                     help="skip the energy runs (8 s of decode and 8 s of prefill, amdsmi counter)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -1191,7 +1399,8 @@ def main():
     if args.calibrate_copy:
         copy_calibration()
     if args.only and args.only != "decode":
-        fn = {"extend": bench_extend, "prefill": bench_prefill_transfer, "mixed": bench_mixed,
+        fn = {"extend": bench_extend, "prefill": bench_prefill_transfer,
+              "mixed": lambda a: bench_mixed(a, collocated=a.mixed_collocated),
               "prefill1": lambda a: bench_prefill_transfer(a, parts=("prefill",)),
               "transfer": lambda a: bench_prefill_transfer(a, parts=("transfer",)),
               "append": bench_append, "device": lambda a: {"device": device_block(), "host": host_info()},
@@ -1212,6 +1421,7 @@ def main():
         comps.update(bench_decode_curve(args))
         if args.mixed_steps > 0:
             comps.update(bench_mixed(args))
+            comps.update(bench_mixed(args, collocated=True))
         comps.update(bench_sim(comps))
     split_gbs = dec["split_bytes"] / (dec["split_ms"] * 1e-3) / 1e9
     line = {
