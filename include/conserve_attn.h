@@ -222,6 +222,14 @@ cs_status cs_mixed_step(cs_pool* pool, int32_t n_ext, const cs_conv* ext_convs,
                         const void* k, const void* v, const void* q_ext, void* out_ext,
                         const void* q_dec, void* out_dec, uint32_t flags, cs_stream stream);
 
+/*
+ * Version of the transfer wire format of cs_kv_pack / cs_kv_unpack below. The format is frozen at
+ * this version: it is the pool's block format as of version 1, and a later change of the pool's
+ * private block layout keeps pack and unpack reading and writing exactly this format (a new format
+ * would take a new version number).
+ */
+#define CS_WIRE_FORMAT_VERSION 1
+
 /* Wire size of a conversation's KV: n_layers * ceil(len/16) * n_kv_heads * 64 * head_dim bytes. */
 cs_status cs_kv_pack_size(const cs_pool* pool, cs_conv conv, size_t* bytes);
 

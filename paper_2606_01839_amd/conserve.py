@@ -21,6 +21,7 @@ STATUS_NAMES = {CS_EINVAL: "CS_EINVAL", CS_ENOMEM: "CS_ENOMEM", CS_ENOENT: "CS_E
                 CS_ESTATE: "CS_ESTATE", CS_ERANGE: "CS_ERANGE", CS_EHIP: "CS_EHIP",
                 CS_EBUSY: "CS_EBUSY"}
 PAGE_TOKENS = 16
+WIRE_FORMAT_VERSION = 1       # CS_WIRE_FORMAT_VERSION: the frozen layout of kv_pack / kv_unpack
 
 EXPORTS = [
     "cs_pool_kv_bytes", "cs_pool_workspace_bytes", "cs_pool_create", "cs_pool_destroy",

@@ -30,6 +30,14 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, n), n
 
 
+def test_wire_format_version_matches_the_header():
+    """The binding's wire-format version is the header's (the layout the golden fixtures pin)."""
+    from paper_2606_01839_amd import conserve
+    src = open(os.path.join(ROOT, "include", "conserve_attn.h")).read()
+    m = re.search(r"#define\s+CS_WIRE_FORMAT_VERSION\s+(\d+)", src)
+    assert m and int(m.group(1)) == conserve.WIRE_FORMAT_VERSION == 1
+
+
 def _pool(**kw):
     from paper_2606_01839_amd import KVPool
     args = dict(n_layers=1, n_q_heads=4, n_kv_heads=2, head_dim=64, n_pages=32, max_convs=3,
