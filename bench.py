@@ -929,7 +929,8 @@ def bench_mixed(args, collocated=False):
     memory, destroyed) and later swapped back in (kv_unpack) before anything new is admitted.
 
     With --mixed-to-completion the run continues until every conversation has completed, in the
-    layer-ordered form of the step (a model forward pass), sampling oracle parity every 2000 steps;
+    layer-ordered form of the step (a model forward pass) except every 25th step, which runs in the
+    overlapped order with per-kernel timing events, sampling oracle parity every 2000 steps;
     otherwise `args.mixed_steps` timed steps alternate between the two orders of cs_mixed_step.
 
     collocated=True is the paper's collocated baseline instead (Section 5.1): no prefiller; a new
@@ -1086,6 +1087,7 @@ def bench_mixed(args, collocated=False):
     steplog = []     # layer-ordered timed steps: (seconds, decode tokens, prompt chunk tokens, append tokens)
     want_check = False
     check_every = int(getattr(args, "mixed_check_every", 2000))
+    sample_every = 25
     max_steps = 10 ** 7 if to_completion else args.mixed_steps + 1
     max_s = getattr(args, "mixed_max_s", None)
     stop = [False]
@@ -1141,7 +1143,12 @@ def bench_mixed(args, collocated=False):
         qd = rows_all(KIND_Q, items_new[len(ext):], hq) if dcs else None
         torch.cuda.synchronize()
         timed_step = step > 0                                      # step 0 warms up
-        ordered = True if (to_completion or collocated) else step % 2 == 0
+        # to completion: every sample_every-th step runs in the overlapped order with per-kernel
+        # timing events, which samples the decode and extend rates over the whole run
+        if to_completion:
+            ordered = step % sample_every != 0
+        else:
+            ordered = True if collocated else step % 2 == 0
         acc = tot_ord if ordered else tot
         if timed_step and not ordered:
             dec.profile_start()
@@ -1265,7 +1272,7 @@ def bench_mixed(args, collocated=False):
             "step_roofline": {"frac": roof_s(t) / t["wall_s"] if t["wall_s"] else None},
             "spot_parity": parity}}
     if to_completion:
-        t = tot_ord
+        t = {k_: tot[k_] + tot_ord[k_] for k_ in tot}            # every timed step, both orders
         return {"mixed_to_completion": {
             "workload": workload, "steps": step, "timed_steps": t["steps"], "run_s": run_s,
             "stopped_early": stopped_early,
@@ -1277,6 +1284,18 @@ def bench_mixed(args, collocated=False):
             "step_ms": 1e3 * t["wall_s"] / max(1, t["steps"]),
             "step_roofline": {"roofline_s": roof_s(t), "measured_step_s": t["wall_s"],
                               "frac": roof_s(t) / t["wall_s"] if t["wall_s"] else None},
+            "sampled_kernel_rates": {
+                "steps": tot["steps"],
+                "note": f"every {sample_every}th step runs in the overlapped order with per-kernel "
+                        "timing events (all other steps are layer-ordered, without events); rates "
+                        "use each kernel kind's event-timed duration, which includes the time the "
+                        "two streams share the GPU",
+                "decode_gbs": gbs(tot["dec_bytes"], tot["split_ms"] + tot["merge_ms"]),
+                "decode_split_gbs": gbs(tot["dec_bytes"], tot["split_ms"]),
+                "extend_tflops": tfs(tot["ext_flops"], tot["fwd_ms"]),
+                "append_gbs": gbs(tot["append_bytes"], tot["append_ms"]),
+                "step_ms": 1e3 * tot["wall_s"] / max(1, tot["steps"]),
+                "step_roofline_frac": roof_s(tot) / tot["wall_s"] if tot["wall_s"] else None},
             "turn1_prefill_tflops": tfs(stats["prefill_flops"], stats["prefill_ms"]),
             "pack_gbs": gbs(stats["move_bytes"], stats["pack_ms"]),
             "unpack_gbs": gbs(stats["move_bytes"], stats["unpack_ms"]),

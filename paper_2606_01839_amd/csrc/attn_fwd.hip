@@ -66,8 +66,11 @@ constexpr float kSumLimit = 256.f;
 
 // ------------------------------------------------------------------------------------------------
 // head_dim 128: K/V copied from HBM straight into LDS.
-// LDS layout of one ring buffer (32 KiB): K as 64 rows x 256 B, the 16-byte chunk index XOR-swizzled
-// by the row (chunk ^ (row & 15)); V^T page by page, 128 dims x 32 B (16 keys) per page, the two
+// LDS ring of four tiles: the K parts of the four buffers in the low 64 KiB (16 KiB each), their
+// V^T parts in the high 64 KiB, so every operand read reaches its buffer through the instruction's
+// 16-bit offset field (no address arithmetic per read). K as 64 rows x 256 B, the 16-byte chunk
+// index XOR-swizzled by the row (chunk ^ (row & 15)); V^T page by page, 128 dims x 32 B (16 keys)
+// per page, the two
 // 16-byte halves of a dim swapped when bit 2 xor bit 3 of the dim is set. A 16-byte operand read
 // is served 16 lanes at a time over 256 bytes of banks: the 16 rows (K) or dims (V^T) such a group
 // reads then fall in 16 distinct 16-byte bank groups (rocprofv3 SQ_LDS_BANK_CONFLICT = 0), while
@@ -103,9 +106,10 @@ __device__ __forceinline__ void attn_fwd_block(const ExtendArgs& a, const int bl
   constexpr int NB = 16;                  // 1 KiB blocks per K (and per V^T) tile
   constexpr int BPW = NB / NW;            // blocks per wave
   static_assert(NB % NW == 0 && BPW <= 4, "a wave's blocks must lie in one page");
-  constexpr int TILE = 32768;             // K + V^T bytes per buffer
+  constexpr int HALF_TILE = 16384;        // K (or V^T) bytes per buffer
   constexpr int NBUF = 4;                 // LDS ring: tile j read, j+1 landed, j+2 and j+3 in flight
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[NBUF * TILE];
+  constexpr int VBASE = NBUF * HALF_TILE; // V^T parts after the K parts of all buffers
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * NBUF * HALF_TILE];
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int tile_idx = block / a.n_kv_heads, g = block % a.n_kv_heads;
@@ -153,8 +157,8 @@ __device__ __forceinline__ void attn_fwd_block(const ExtendArgs& a, const int bl
 #pragma unroll
     for (int i = 0; i < BPW; ++i) {
       const int kb = BPW * wave + i;
-      dma16(smem_base + buf * TILE + kb * 1024, blk, koff[i]);
-      dma16(smem_base + buf * TILE + 16384 + kb * 1024, blk, voff[i]);
+      dma16(smem_base + buf * HALF_TILE + kb * 1024, blk, koff[i]);
+      dma16(smem_base + VBASE + buf * HALF_TILE + kb * 1024, blk, voff[i]);
     }
   };
 
@@ -169,7 +173,7 @@ __device__ __forceinline__ void attn_fwd_block(const ExtendArgs& a, const int bl
   for (int ks = 0; ks < KS; ++ks)
     kaddr[ks] = static_cast<uint32_t>(col * (2 * D) + (((2 * ks + half) ^ (col & 15)) * 16));
   const uint32_t vaddr =
-      static_cast<uint32_t>(16384 + col * 32 + ((half ^ ((col >> 2) & 1) ^ ((col >> 3) & 1)) * 16));
+      static_cast<uint32_t>(col * 32 + ((half ^ ((col >> 2) & 1) ^ ((col >> 3) & 1)) * 16));
 
   bf16x8 qop[KS];
   int qpos;
@@ -206,7 +210,7 @@ __device__ __forceinline__ void attn_fwd_block(const ExtendArgs& a, const int bl
   // K operands of the next tile are read into registers during the current tile's PV product.
   bf16x8 kop[KS][2];
   auto read_k = [&](int buf) {
-    const uint8_t* kb = smem + buf * TILE;
+    const uint8_t* kb = smem + buf * HALF_TILE;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
@@ -217,7 +221,7 @@ __device__ __forceinline__ void attn_fwd_block(const ExtendArgs& a, const int bl
 
   auto tile_step = [&](const int j, const int buf) {
     copy_tile(min(j + 3, n_kt - 1), (buf + 3) % NBUF);
-    const uint8_t* kb = smem + buf * TILE;
+    const uint8_t* vb = smem + VBASE + buf * HALF_TILE;
     f32x16 s[2];
 #pragma unroll
     for (int kt2 = 0; kt2 < 2; ++kt2)
@@ -236,7 +240,7 @@ __device__ __forceinline__ void attn_fwd_block(const ExtendArgs& a, const int bl
       for (int j2 = 0; j2 < 2; ++j2)
 #pragma unroll
         for (int t = 0; t < DT; ++t)
-          vop[kt2][j2][t] = as_bf16x8(ld16(kb + vaddr + (4 * (2 * kt2 + j2) + t) * 1024));
+          vop[kt2][j2][t] = as_bf16x8(ld16(vb + vaddr + (4 * (2 * kt2 + j2) + t) * 1024));
 
     if (kBN * j + kBN - 1 > pos_min) {
 #pragma unroll
