@@ -1409,7 +1409,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the hot path shards by conversation with no exchange "
-              "on the hot path, and this build runs on a single MI355X (use --gpus 1).", file=sys.stderr)
+              "on the hot path, and this benchmark runs on a single MI355X (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
