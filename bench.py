@@ -1229,7 +1229,9 @@ def bench_mixed(args, collocated=False):
             log(f"mixed: step {step}, {stats['completed']} completed, {len(live)} live, "
                 f"{len(swapped)} swapped, {len(queue)} waiting, {time.perf_counter() - t_run:.0f}s")
     run_s = time.perf_counter() - t_run
-    signal.signal(signal.SIGTERM, old_term)
+    # a handler installed outside Python (a profiler's, for one) reads back as None: restore the
+    # default then
+    signal.signal(signal.SIGTERM, old_term if old_term is not None else signal.SIG_DFL)
     stopped_early = bool(live or swapped or queue) and to_completion
     used, free_pages = dec.occupancy()
     sched.close()
