@@ -911,7 +911,7 @@ ADMIT_WATERMARK = 0.8    # bind only while the decoder's pages after the transfe
 COLLOCATED_BUDGET = 2944   # tokens per step of the paper's collocated replicas (Section 5.1)
 
 
-def bench_mixed(args, collocated=False):
+def bench_mixed(args, collocated=False, trace_cfg=None, pool_pages=None):
     """Serve the synthetic agentic trace on one decoder pool (Section 4: after the one-time
     transfer a conversation's later turns run on its decoder).
 
@@ -936,9 +936,12 @@ def bench_mixed(args, collocated=False):
     collocated=True is the paper's collocated baseline instead (Section 5.1): no prefiller; a new
     conversation's turn-1 prompt is prefilled on the decoder itself in chunks, batched with the
     decodes under a budget of COLLOCATED_BUDGET tokens per step (decode tokens first, then prompt
-    and append chunks in admission order, split as the budget allows), layer-ordered steps."""
+    and append chunks in admission order, split as the budget allows), layer-ordered steps.
+
+    trace_cfg (a synth.traces.MixedTrace) and pool_pages (decoder pool size in pages) replace the
+    256-conversation trace and the HBM-sized pool, for small runs of the same serving loop."""
     from paper_2606_01839_amd import KVPool, Scheduler
-    tr = MixedTrace()
+    tr = trace_cfg if trace_cfg is not None else MixedTrace()
     sh = tr.shape
     NL, hq, hkv, d = sh.n_layers, sh.n_q_heads, sh.n_kv_heads, sh.head_dim
     trace = tr.conversations()
@@ -951,7 +954,7 @@ def bench_mixed(args, collocated=False):
     free, _ = torch.cuda.mem_get_info()
     max_t1 = max(c.turn1 for c in trace)
     reserve = 3 * pages_for(max_t1) * page_bytes + (24 << 30)    # prefiller, wire, step buffers
-    n_pages = int((0.85 * free - reserve) // page_bytes)
+    n_pages = int((0.85 * free - reserve) // page_bytes) if pool_pages is None else int(pool_pages)
     max_final = max(c.final_len() for c in trace)
     dec = KVPool(NL, hq, hkv, d, n_pages=n_pages, max_convs=tr.n_convs,
                  max_pages_per_conv=pages_for(max_final), placement_seed=tr.seed + 1)
